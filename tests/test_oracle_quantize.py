@@ -1,0 +1,162 @@
+"""Pins for the oracle's normalize / encode / pack / qlinear (CPU only).
+
+Independent anchors: brute-force nearest-centroid search (Eq. (3) written as an
+argmin over all levels), hand-computed packed bytes, exact scale invariance of
+the normalized code, the zero-row guard of Sec. 4.3, the closed form of a
+constant-code product, the rotation cancellation with an identity quantizer,
+and the statistical error band sqrt(D_w + D_a) of independent Lloyd-Max
+quantizers (a band, not parity).
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+from hypothesis import given, settings, strategies as st
+
+import oracle
+from paper_2607_02461_amd import workloads
+
+
+def _cb(bits, d):
+    return oracle.lloydmax_codebook(bits, d)
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.integers(2, 4), st.sampled_from([64, 3072, 13824]),
+       st.lists(st.floats(-0.2, 0.2, allow_nan=False), min_size=1, max_size=40))
+def test_encode_is_bruteforce_argmin_off_ties(bits, d, us):
+    cb = _cb(bits, d)
+    u = np.array(us)
+    codes = oracle.encode(u, cb.thresholds)
+    dist = np.abs(u[:, None] - cb.levels[None, :])
+    brute = np.argmin(dist, axis=1)
+    ok = ~oracle.near_tie_mask(u, cb.thresholds, 1e-12)
+    assert np.array_equal(codes[ok], brute[ok])
+
+
+def test_encode_tie_takes_upper_code():
+    cb = _cb(2, 3072)
+    codes = oracle.encode(cb.thresholds, cb.thresholds)
+    assert np.array_equal(codes, np.arange(1, 4))
+
+
+def test_encode_sign_symmetry_off_ties():
+    cb = _cb(4, 3072)
+    u = np.random.default_rng(0).normal(size=5000) / math.sqrt(3072)
+    ok = ~oracle.near_tie_mask(u, cb.thresholds, 1e-12)
+    c, cn = oracle.encode(u, cb.thresholds), oracle.encode(-u, cb.thresholds)
+    assert np.array_equal(cn[ok], 15 - c[ok])
+
+
+def test_pack_hand_computed_bytes():
+    # b=4: code k in bits [4k, 4k+4): (1,2)->0x21 (3,4)->0x43 (15,0)->0x0F (7,8)->0x87
+    p4 = oracle.pack_codes(np.array([[1, 2, 3, 4, 15, 0, 7, 8]]), 4)
+    assert p4.tolist() == [[0x21, 0x43, 0x0F, 0x87]]
+    # b=2: (0,1,2,3) -> 0b11100100 = 0xE4 ; (3,2,1,0) -> 0b00011011 = 0x1B
+    p2 = oracle.pack_codes(np.array([[0, 1, 2, 3, 3, 2, 1, 0]]), 2)
+    assert p2.tolist() == [[0xE4, 0x1B]]
+    # b=3: sum_k code_k << 3k for (5,3,7,0,1,6,2,4) = 9114077 = 0x8B11DD, little-endian bytes
+    p3 = oracle.pack_codes(np.array([[5, 3, 7, 0, 1, 6, 2, 4]]), 3)
+    assert p3.tolist() == [[0xDD, 0x11, 0x8B]]
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_pack_roundtrip(bits):
+    rng = np.random.default_rng(bits)
+    codes = rng.integers(0, 1 << bits, size=(7, 256))
+    packed = oracle.pack_codes(codes, bits)
+    assert packed.shape == (7, 256 * bits // 8)
+    assert np.array_equal(oracle.unpack_codes(packed, bits, 256), codes)
+
+
+def test_bf16_round_known_values_and_library():
+    assert oracle.bf16_round(1.0) == 1.0
+    assert oracle.bf16_round(1.0 + 2 ** -8) == 1.0                  # tie -> even
+    assert oracle.bf16_round(1.0 + 3 * 2 ** -8) == 1.0 + 2 ** -6    # tie -> even (up)
+    assert oracle.bf16_round(1.0 + 2 ** -8 + 2 ** -20) == 1.0 + 2 ** -7
+    # fp32-exact values agree with torch's fp32 -> bf16 conversion
+    v = np.random.default_rng(1).normal(size=2000).astype(np.float32).astype(np.float64) * 7.3
+    t = torch.tensor(v, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(oracle.bf16_round(v), t)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_scale_invariance_is_exact(bits):
+    X, _ = workloads.c1_inputs()
+    X = X[:16].float().numpy().astype(np.float64)
+    plan = oracle.rpbh_plan(3072, 128, 0)
+    cb = _cb(bits, 3072)
+    c0, s0, _ = oracle.quantize_act(X, plan, cb, eps=0.0)
+    for k in (-7, 3, 11):
+        ck, sk, _ = oracle.quantize_act(X * 2.0 ** k, plan, cb, eps=0.0)
+        assert np.array_equal(ck, c0)
+        assert np.array_equal(sk, s0 * 2.0 ** k)
+
+
+def test_zero_row_guard():
+    plan = oracle.rpbh_plan(256, 128, 0)
+    for bits in (2, 3, 4):
+        cb = _cb(bits, 256)
+        X = np.zeros((2, 256))
+        X[1, 5] = 3.0
+        c, s, u = oracle.quantize_act(X, plan, cb)
+        assert s[0] == 0.0 and np.all(u[0] == 0.0)
+        assert np.all(c[0] == (1 << (bits - 1)))       # u = 0 sits on the middle threshold
+        cw, r, _ = oracle.quantize_weights(X, plan, cb)
+        assert r[0] == 0.0 and r[1] == 3.0
+
+
+def test_qlinear_constant_codes_closed_form():
+    rng = np.random.default_rng(3)
+    La, Lw = np.sort(rng.normal(size=16)), np.sort(rng.normal(size=8))
+    M, N, K = 3, 4, 40
+    s, r = rng.uniform(0.5, 2, M), rng.uniform(0.5, 2, N)
+    Y = oracle.qlinear(np.full((M, K), 5), s, La, np.full((N, K), 2), r, Lw)
+    assert np.allclose(Y, s[:, None] * r[None, :] * K * La[5] * Lw[2], rtol=1e-14)
+
+
+def test_qlinear_matches_triple_loop():
+    rng = np.random.default_rng(4)
+    La, Lw = rng.normal(size=4), rng.normal(size=8)
+    cx, cw = rng.integers(0, 4, (3, 6)), rng.integers(0, 8, (2, 6))
+    s, r = rng.uniform(1, 2, 3), rng.uniform(1, 2, 2)
+    Y = oracle.qlinear(cx, s, La, cw, r, Lw)
+    for n in range(3):
+        for i in range(2):
+            want = s[n] * r[i] * sum(La[cx[n, k]] * Lw[cw[i, k]] for k in range(6))
+            assert abs(Y[n, i] - want) < 1e-13
+
+
+def test_qlinear_with_identity_quantizer_recovers_dense_layer():
+    # an exact "codebook" (one level per coordinate) turns qlinear into W'x' = Wx (Sec. 4.3)
+    rng = np.random.default_rng(5)
+    M, N, d = 4, 3, 256
+    X, W = rng.normal(size=(M, d)), rng.normal(size=(N, d))
+    plan = oracle.rpbh_plan(d, 128, 7)
+    zx, zw = oracle.rpbh_forward(X, plan), oracle.rpbh_forward(W, plan)
+    s, ux = oracle.normalize_rows(zx, 0.0)
+    r, uw = oracle.normalize_rows(zw, 0.0)
+    Y = oracle.qlinear(np.arange(M * d).reshape(M, d), s, ux.ravel(),
+                       np.arange(N * d).reshape(N, d), r, uw.ravel())
+    assert np.max(np.abs(Y - X @ W.T)) < 1e-11
+
+
+@pytest.mark.parametrize("bw,ba,lo,hi", [(4, 4, 0.11, 0.19), (3, 4, 0.17, 0.26),
+                                         (2, 4, 0.31, 0.42), (3, 3, 0.22, 0.32)])
+def test_end_to_end_error_band(bw, ba, lo, hi):
+    # statistical: independent Lloyd-Max quantizers of both operands give a relative
+    # Frobenius error near sqrt(D_bw + D_ba) (Max's distortions), here on outlier data
+    X, W = workloads.c1_inputs()
+    X = X[:48].double().numpy()
+    W = W[:192].double().numpy()
+    d = 3072
+    plan = oracle.rpbh_plan(d, 128, 0)
+    cba, cbw = _cb(ba, d), _cb(bw, d)
+    cx, s, _ = oracle.quantize_act(X, plan, cba)
+    cw, r, _ = oracle.quantize_weights(W, plan, cbw)
+    Y = oracle.qlinear(cx, s, cba.levels, cw, r, cbw.levels)
+    ref = oracle.qlinear_dense_reference(X, W)
+    err = np.linalg.norm(Y - ref) / np.linalg.norm(ref)
+    assert lo < err < hi, err
