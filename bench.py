@@ -1,0 +1,271 @@
+"""Benchmark of the OrbitQuant quantized-linear hot path on one MI355X.
+
+A step is one pass of the online path over one batch: for each linear of the workload the
+fused RPBH activation quantizer (rpbh_quantize_act) followed by the LUT-decode GEMM
+(orbit_qlinear), on inputs already resident in HBM.  The offline weight pass
+(quantize_weights_offline) and the host-side plan/codebook construction are timed once,
+separately, and reported beside the step.
+
+Default workload: the video-DiT MLP, W4A4, 32760 latent-patch + 512 text tokens,
+5120 -> 13824 -> 5120 (two quantized linears per step).
+
+Prints ONE JSON line (rank 0).  Kernel durations come from HIP events recorded on the stream
+the kernels are launched on (torch's current stream).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "orbit_qlinear TFLOP/s + rpbh_quantize_act GB/s (% of MI355X roofline)"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c4_video_mlp_w4a4", choices=["c4_video_mlp_w4a4", "c1_single_w4a4"])
+    ap.add_argument("--cpu-baseline-rows", type=int, default=2048,
+                    help="token rows of the oracle's timed CPU sample (0 disables it)")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="per-kernel HBM bytes measured with rocprofv3 counters (optional)")
+    return ap.parse_args()
+
+
+def quant_bytes(M, K, bits):
+    """Algorithmic bytes of one quantizer launch: bf16 rows in, packed codes + fp32 norms out."""
+    return M * (2 * K + K * bits // 8 + 4)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1 "
+                                   "(rows shard across GPUs with no exchange, see the design notes)"}))
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(2)
+
+    import paper_2607_02461_amd as oq
+    from paper_2607_02461_amd import workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = workloads.WORKLOADS[args.workload]
+
+    # ---- inputs (synthetic, seeded) ------------------------------------------------------
+    if wl is workloads.C4:
+        Xu, Xd, Wu, Wd = workloads.c4_inputs(device=dev)
+        lin_inputs = [(wl.linears[0], Xu, Wu), (wl.linears[1], Xd, Wd)]
+    else:
+        X, W = workloads.c1_inputs(device=dev)
+        lin_inputs = [(wl.linears[0], X, W)]
+    torch.cuda.synchronize()
+
+    # ---- offline stage: plans + codebooks on the host, weight pass on the GPU -------------
+    t0 = time.perf_counter()
+    plans, cbs = {}, {}
+    for lin, _, _ in lin_inputs:
+        plans[lin.K] = oq.rpbh_plan(lin.K, lin.h, wl.plan_seed)
+        cbs[(lin.ba, lin.K)] = oq.lloydmax_codebook(lin.ba, lin.K)
+        cbs[(lin.bw, lin.K)] = oq.lloydmax_codebook(lin.bw, lin.K)
+    host_offline_s = time.perf_counter() - t0
+
+    layers = []
+    for lin, X, W in lin_inputs:
+        wc = torch.empty((lin.N, lin.K * lin.bw // 8), dtype=torch.uint8, device=dev)
+        wn = torch.empty((lin.N,), dtype=torch.bfloat16, device=dev)
+        xc = torch.empty((lin.M, lin.K * lin.ba // 8), dtype=torch.uint8, device=dev)
+        xn = torch.empty((lin.M,), dtype=torch.float32, device=dev)
+        Y = torch.empty((lin.M, lin.N), dtype=torch.float32, device=dev)
+        layers.append(dict(lin=lin, X=X, W=W, wc=wc, wn=wn, xc=xc, xn=xn, Y=Y,
+                           plan=plans[lin.K], cba=cbs[(lin.ba, lin.K)], cbw=cbs[(lin.bw, lin.K)]))
+
+    def weight_pass():
+        for L in layers:
+            oq.quantize_weights_offline(L["plan"], L["cbw"], L["W"], 1e-10, L["wc"], L["wn"])
+
+    weight_pass()  # also uploads the plan tables
+    torch.cuda.synchronize()
+    wp_reps = 5
+    ws, we = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ws.record()
+    for _ in range(wp_reps):
+        weight_pass()
+    we.record()
+    torch.cuda.synchronize()
+    weight_pass_ms = ws.elapsed_time(we) / wp_reps
+    weight_bytes = sum(L["lin"].N * (2 * L["lin"].K + L["lin"].K * L["lin"].bw // 8 + 2) for L in layers)
+
+    # ---- the step --------------------------------------------------------------------------
+    nl = len(layers)
+
+    def step(ev=None):
+        for i, L in enumerate(layers):
+            if ev is not None:
+                ev[4 * i].record()
+            oq.rpbh_quantize_act(L["plan"], L["cba"], L["X"], 1e-10, L["xc"], L["xn"])
+            if ev is not None:
+                ev[4 * i + 1].record()
+                ev[4 * i + 2].record()
+            oq.orbit_qlinear(L["cba"], L["xc"], L["xn"], L["cbw"], L["wc"], L["wn"], L["Y"])
+            if ev is not None:
+                ev[4 * i + 3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4 * nl)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    start.record()
+    for s in range(args.steps):
+        step(events[s])
+    end.record()
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t_wall0
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+
+    quant_ms = np.zeros(nl)
+    gemm_ms = np.zeros(nl)
+    for ev in events:
+        for i in range(nl):
+            quant_ms[i] += ev[4 * i].elapsed_time(ev[4 * i + 1])
+            gemm_ms[i] += ev[4 * i + 2].elapsed_time(ev[4 * i + 3])
+    quant_ms /= args.steps
+    gemm_ms /= args.steps
+
+    flops = np.array([2.0 * L["lin"].M * L["lin"].N * L["lin"].K for L in layers])
+    qbytes = np.array([quant_bytes(L["lin"].M, L["lin"].K, L["lin"].ba) for L in layers], dtype=np.float64)
+    gemm_tflops = flops.sum() / (gemm_ms.sum() * 1e-3) / 1e12
+    quant_gbs = qbytes.sum() / (quant_ms.sum() * 1e-3) / 1e9
+    step_tflops = flops.sum() / (ms_per_step * 1e-3) / 1e12
+
+    traffic = None
+    if os.path.exists(args.traffic):
+        try:
+            t = json.load(open(args.traffic))
+            if t.get("workload") == wl.name:
+                traffic = t
+        except (OSError, ValueError):
+            traffic = None
+
+    gemm_launch_flops = float(flops.mean())
+    gemm_avg_ms = float(gemm_ms.mean())
+    roofline = {
+        "kernel": "lut_gemm_kernel<4,4>" if all(L["lin"].ba == 4 and L["lin"].bw == 4 for L in layers) else "lut_gemm_kernel",
+        "bound": "mfma",
+        "achieved": gemm_launch_flops / (gemm_avg_ms * 1e-3) / 1e12,
+        "peak": FP16_MFMA_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": gemm_launch_flops / (gemm_avg_ms * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS,
+        "traffic": (traffic or {}).get("gemm_bytes_per_launch"),
+        "avg_launch_ms": gemm_avg_ms,
+        "algorithmic_flops_per_launch": gemm_launch_flops,
+    }
+    roofline_q = {
+        "kernel": "rpbh_quantize_kernel",
+        "bound": "hbm",
+        "achieved": quant_gbs,
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": quant_gbs / HBM_PEAK_GBS,
+        "traffic": (traffic or {}).get("quant_bytes_per_launch"),
+        "avg_launch_ms": [float(v) for v in quant_ms],
+        "algorithmic_bytes_per_launch": [float(v) for v in qbytes],
+    }
+
+    cpu = None
+    if args.cpu_baseline_rows > 0:
+        cpu = cpu_baseline(layers, args.cpu_baseline_rows)
+
+    out = {
+        "metric": METRIC,
+        "value": step_tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "description": wl.description,
+            "linears": [{"name": L["lin"].name, "M": L["lin"].M, "K": L["lin"].K, "N": L["lin"].N,
+                         "bits": f"W{L['lin'].bw}A{L['lin'].ba}", "h": L["lin"].h} for L in layers],
+            "value_is": "GEMM flops of the step / step time (quantizer + GEMM per linear)",
+            "arith": "quantizer fp32; GEMM fp16 MFMA operands, fp32 accumulate",
+        },
+        "components": {
+            "orbit_qlinear_tflops": gemm_tflops,
+            "orbit_qlinear_frac_of_fp16_peak": gemm_tflops / FP16_MFMA_PEAK_TFLOPS,
+            "rpbh_quantize_act_gbs": quant_gbs,
+            "rpbh_quantize_act_frac_of_hbm": quant_gbs / HBM_PEAK_GBS,
+            "quant_ms": [float(v) for v in quant_ms],
+            "gemm_ms": [float(v) for v in gemm_ms],
+            "weight_pass_ms": weight_pass_ms,
+            "weight_pass_gbs": weight_bytes / (weight_pass_ms * 1e-3) / 1e9,
+            "host_plan_codebook_s": host_offline_s,
+            "wall_s_timed_region": wall_s,
+        },
+        "roofline": roofline,
+        "roofline_quantizer": roofline_q,
+        "cpu_baseline": cpu,
+        "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0)},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(layers, rows):
+    """The fp64 oracle timed on the host cores on a bounded sample: `rows` token rows through
+    every linear of the step (quantize + contraction).  The oracle's weight codes are made
+    once, outside the timing, as the GPU's offline weight pass is outside the step."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = os.cpu_count()
+    prepared = []
+    for L in layers:
+        lin = L["lin"]
+        plan = oracle.rpbh_plan(lin.K, lin.h, 0)
+        cba, cbw = oracle.lloydmax_codebook(lin.ba, lin.K), oracle.lloydmax_codebook(lin.bw, lin.K)
+        W = L["W"].float().cpu().numpy().astype(np.float64)
+        cw, r, _ = oracle.quantize_weights(W, plan, cbw)
+        del W
+        X = L["X"][:rows].float().cpu().numpy().astype(np.float64)
+        prepared.append((lin, plan, cba, cbw, cw, r, X))
+    t0 = time.perf_counter()
+    flops = 0.0
+    for lin, plan, cba, cbw, cw, r, X in prepared:
+        cx, s, _ = oracle.quantize_act(X, plan, cba)
+        oracle.qlinear(cx, s, cba.levels, cw, r, cbw.levels)
+        flops += 2.0 * X.shape[0] * lin.N * lin.K
+    dt = time.perf_counter() - t0
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": blas_threads, "kind": "oracle",
+            "sample": f"{rows} token rows through every linear of the step (quantize + fp64 contraction), "
+                      f"{dt:.1f} s; same metric unit as the GPU value",
+            "seconds": dt}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,193 @@
+/*
+ * orbitquant.h -- C ABI of the OrbitQuant quantized-linear hot path on MI355X (gfx950).
+ *
+ * OrbitQuant (arXiv 2607.02461) quantizes a linear layer y = W x (Sec. 3.1, Eq. (1)) of a
+ * diffusion transformer without calibration data.  Weights and activations are rotated by
+ * the same randomized permuted block-Hadamard (RPBH) transform Pi_d (Sec. 4.4, Eq. (9)),
+ * split into a norm and a unit direction, and the direction is encoded coordinate-wise
+ * against one fixed Lloyd-Max codebook per (input dimension d, bit-width b) fitted to the
+ * rotated-coordinate marginal f_d (Sec. 3.2, Eqs. (2)-(3)).  The rotation cancels inside
+ * the product (Sec. 4.3), so the layer contracts the two code sets directly.
+ *
+ * Conventions shared by every call
+ *   - Every function returns orbit_status; 0 is success.  Nothing throws across the ABI.
+ *     On failure orbit_last_error() returns a message for the calling thread, valid until
+ *     that thread's next call into the library.
+ *   - BF16 values are passed as uint16_t bit patterns; fp32 as float.
+ *   - Matrices are row-major with the reduction dimension K contiguous.
+ *   - Packed codes: an LSB-first bit stream per row; the code of coordinate k occupies bits
+ *     [k*b, k*b + b) of the row, so a row of K codes is K*b/8 bytes and rows are contiguous.
+ *     A code is the index of its level in the ascending level list (0 = most negative).
+ *   - Device calls take device pointers the caller owns (e.g. torch tensors), only enqueue
+ *     work on `stream` (a hipStream_t; NULL = the null stream) and return before it runs.
+ *     They allocate no device memory for their operands.  Argument checks are synchronous
+ *     and happen before any launch; a launch failure returns ORBIT_EHIP with HIP's message.
+ *   - Handles are immutable after creation and may be used from several threads and streams
+ *     at once.  The first device call that uses a plan on a device uploads the plan's
+ *     permutation/sign table to that device (d*4 bytes, hipMalloc + synchronous copy) and
+ *     keeps it until the handle is destroyed.  Destroy a handle only after the work that
+ *     uses it has finished.
+ */
+#ifndef ORBITQUANT_H
+#define ORBITQUANT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ORBIT_OK = 0,
+    ORBIT_EINVAL = 1,        /* an argument is invalid (null, out of range, inconsistent)     */
+    ORBIT_EUNSUPPORTED = 2,  /* valid for the method, but outside what the kernels implement  */
+    ORBIT_ENOMEM = 3,        /* host or device allocation failed                              */
+    ORBIT_EHIP = 4,          /* a HIP runtime call or kernel launch failed                    */
+    ORBIT_EINTERNAL = 5      /* a numerical routine failed to converge or a bug was detected  */
+} orbit_status;
+
+/* Message describing the calling thread's last failure ("" after a success). */
+const char* orbit_last_error(void);
+
+/* Library version string, e.g. "orbitquant-mi355x 0.1.0 gfx950". */
+const char* orbit_version(void);
+
+typedef struct orbit_plan_s* orbit_plan;
+typedef struct orbit_codebook_s* orbit_codebook;
+
+/* ------------------------------------------------------------------ host, offline stage */
+
+/*
+ * rpbh_plan -- draw the RPBH rotation Pi_d = blkdiag(H_h D_1, ..., H_h D_{d/h}) P_pi
+ * (Sec. 4.4, Eq. (9); Alg. 1, offline stage).  Host only; touches no GPU.
+ *
+ *   d     input dimension, >= 1
+ *   h     Hadamard block size: a power of two dividing d; 0 selects the paper's rule,
+ *         the largest power of two dividing d (Sec. 4.4)
+ *   seed  generator seed.  pi and the signs are drawn from SplitMix64 (Steele, Lea &
+ *         Flood 2014) started at state = seed: Fisher-Yates from the identity for
+ *         j = d-1 .. 1 with k uniform in [0, j] (draw u until u >= 2^64 mod (j+1), take
+ *         u mod (j+1)); then sign[j] = -1 when the top bit of the next output is 1.
+ *   out   receives the new handle
+ *
+ * Conventions: (P_pi x)_j = x[perm[j]] (a gather) and sign[j] multiplies the j-th
+ * post-permutation coordinate; H_h is the Sylvester-ordered Walsh-Hadamard matrix scaled
+ * by 1/sqrt(h), so Pi_d is orthogonal.  Errors: ORBIT_EINVAL for d < 1, a bad h or a
+ * null `out`; ORBIT_ENOMEM.
+ */
+orbit_status rpbh_plan(int64_t d, int32_t h, uint64_t seed, orbit_plan* out);
+
+/*
+ * rpbh_plan_from_arrays -- the same handle built from a caller-supplied permutation and
+ * sign vector (host arrays, copied).  perm must be a permutation of 0..d-1, sign entries
+ * must be +1 or -1.  Errors: ORBIT_EINVAL otherwise.
+ */
+orbit_status rpbh_plan_from_arrays(int64_t d, int32_t h, const int32_t* perm, const int8_t* sign,
+                                   orbit_plan* out);
+
+/* Read back a plan.  Any output pointer may be NULL; perm and sign receive d entries. */
+orbit_status rpbh_plan_get(orbit_plan p, int64_t* d, int32_t* h, int32_t* perm, int8_t* sign);
+
+/* Free a plan (host arrays and every per-device copy).  NULL is ignored. */
+void rpbh_plan_destroy(orbit_plan p);
+
+/*
+ * lloydmax_codebook -- the Lloyd-Max codebook C^(d,b) for the marginal
+ * f_d(t) = Gamma(d/2) / (sqrt(pi) Gamma((d-1)/2)) (1 - t^2)^((d-3)/2) on [-1, 1]
+ * (Sec. 3.2, Eqs. (2)-(3); Sec. 4.5; Alg. 1, offline stage).  Host only.
+ *
+ *   bits  1..6 for the codebook itself; the kernels accept 2, 3 and 4
+ *   d     input dimension, >= 3
+ *
+ * Computed in fp64 by the fixed-point iteration of the midpoint and centroid conditions on
+ * the exact f_d (not its Gaussian approximation).  The levels are exactly antisymmetric
+ * and the thresholds are the midpoints of neighbouring levels, so the middle threshold is
+ * exactly 0.  Errors: ORBIT_EINVAL for bits or d out of range; ORBIT_EINTERNAL if the
+ * iteration fails to converge.
+ */
+orbit_status lloydmax_codebook(int32_t bits, int64_t d, orbit_codebook* out);
+
+/*
+ * Read back a codebook: levels (2^b, ascending), thresholds (2^b - 1), and the fp16 image
+ * of the levels that the GEMM decodes to (2^b IEEE half bit patterns, round-to-nearest-even
+ * of the fp64 levels).  Any output pointer may be NULL.
+ */
+orbit_status lloydmax_codebook_get(orbit_codebook c, int32_t* bits, int64_t* d, double* levels,
+                                   double* thresholds, uint16_t* lut_f16);
+
+/* Free a codebook.  NULL is ignored. */
+void lloydmax_codebook_destroy(orbit_codebook c);
+
+/* ------------------------------------------------------------------ device, per call */
+
+/*
+ * quantize_weights_offline -- rotate, normalize and encode weight rows
+ * (Sec. 4.2, Eqs. (4)-(6); Alg. 1, offline stage):
+ *     w'_i = Pi_d w_i,  r'_i = ||w'_i||_2,  code_i = Q_{b_w}(w'_i / (r'_i + eps)),
+ * with r' stored as BF16 (round-to-nearest-even of the fp32 norm).  The codes use the
+ * fp32 norm; only the stored magnitude is rounded.
+ *
+ *   p       plan with plan.d == K
+ *   cb_w    codebook with cb.d == K and cb.bits = b_w in {2, 3, 4}
+ *   W       device, bf16 [N][ldw]; row i is w_i (the layout of nn.Linear.weight)
+ *   N, K    rows and input dimension; N >= 0
+ *   ldw     row stride of W in elements, >= K and a multiple of 8
+ *   eps     guard added to the norm before dividing (1e-10 in the paper; a zero row gives
+ *           r' = 0 and the middle code 2^(b-1) everywhere)
+ *   w_codes device, uint8 [N][K*b_w/8], packed as described above
+ *   w_norm  device, bf16 [N]
+ *   stream  hipStream_t
+ *
+ * Pointers: W and w_codes 16-byte aligned, w_norm 2-byte aligned.
+ * Errors: ORBIT_EINVAL (null pointer, K mismatch, ldw, alignment); ORBIT_EUNSUPPORTED
+ * (h != 128, K > 32768 or bits outside 2..4); ORBIT_EHIP.  N = 0 returns at once.
+ */
+orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const uint16_t* W, int64_t N,
+                                      int64_t K, int64_t ldw, float eps, uint8_t* w_codes,
+                                      uint16_t* w_norm, void* stream);
+
+/*
+ * rpbh_quantize_act -- online activation quantization, one fused kernel
+ * (Sec. 4.3, Eqs. (7)-(8); Alg. 1, online stage):
+ *     x'_n = Pi_d x_n,  s_n = ||x'_n||_2,  code_n = Q_{b_a}(x'_n / (s_n + eps)).
+ *
+ *   X       device, bf16 [M][ldx], tokens as rows
+ *   M, K    tokens and input dimension; M >= 0
+ *   ldx     row stride of X in elements, >= K and a multiple of 8
+ *   eps     as above (1e-10 in the paper)
+ *   x_codes device, uint8 [M][K*b_a/8]
+ *   x_norm  device, fp32 [M]: s_n (the dequantized row is s_n * L_a[code_n])
+ *
+ * Pointers: X and x_codes 16-byte aligned, x_norm 4-byte aligned.
+ * Errors and limits as for quantize_weights_offline.  M = 0 returns at once.
+ */
+orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t* X, int64_t M, int64_t K,
+                               int64_t ldx, float eps, uint8_t* x_codes, float* x_norm, void* stream);
+
+/*
+ * orbit_qlinear -- the quantized layer on codes (Sec. 4.3: W'x' = W Pi^T Pi x = W x; the
+ * codebook GEMM named as future work in the paper's limitations):
+ *     Y[n][i] = x_norm[n] * w_norm[i] * sum_k L_a[x_code[n][k]] * L_w[w_code[i][k]],
+ * where L_a, L_w are the fp16 images of the two codebooks' levels.  Products are exact in
+ * fp32 and accumulate in fp32 on the matrix cores.
+ *
+ *   cb_a, x_codes, x_norm   activation codebook (bits b_a) and the outputs of
+ *                           rpbh_quantize_act for M rows
+ *   cb_w, w_codes, w_norm   weight codebook (bits b_w) and the outputs of
+ *                           quantize_weights_offline for N rows
+ *   K                       input dimension; cb_a.d == cb_w.d == K, K a multiple of 64
+ *   Y                       device, fp32 [M][ldy], ldy >= N
+ *
+ * Pointers: codes 16-byte aligned, x_norm 4-byte, w_norm 2-byte, Y 4-byte aligned.
+ * Errors: ORBIT_EINVAL (null pointer, dimension mismatch, ldy < N); ORBIT_EUNSUPPORTED
+ * (bits outside 2..4, K not a multiple of 64); ORBIT_EHIP.  M = 0 or N = 0 returns at once.
+ */
+orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                           orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
+                           int64_t K, float* Y, int64_t ldy, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ORBITQUANT_H */

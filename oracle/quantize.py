@@ -51,9 +51,15 @@ def encode(U: np.ndarray, thresholds: np.ndarray) -> np.ndarray:
 
 
 def near_tie_mask(U: np.ndarray, thresholds: np.ndarray, band: float) -> np.ndarray:
-    """True where a coordinate lies within `band` of some decision threshold."""
-    dist = np.min(np.abs(np.asarray(U)[..., None] - thresholds), axis=-1)
-    return dist <= band
+    """True where a coordinate lies within `band` of some decision threshold.
+
+    The thresholds are sorted, so the nearest one is a neighbour of the insertion point."""
+    U = np.asarray(U, dtype=np.float64)
+    t = np.asarray(thresholds, dtype=np.float64)
+    idx = np.searchsorted(t, U)
+    lo = np.abs(U - t[np.clip(idx - 1, 0, len(t) - 1)])
+    hi = np.abs(U - t[np.clip(idx, 0, len(t) - 1)])
+    return np.minimum(lo, hi) <= band
 
 
 def decode_levels(codes: np.ndarray, levels: np.ndarray) -> np.ndarray:

@@ -1,0 +1,225 @@
+"""OrbitQuant quantized linear layer on MI355X (gfx950): Python binding of liborbitquant.so.
+
+The binding only marshals arguments: it allocates outputs with torch on the input's device,
+passes raw pointers and torch's current HIP stream to the C ABI (include/orbitquant.h), and
+raises on any non-zero status.  Every step of the hot path runs in the library's kernels;
+there is no fallback: if the library is missing, importing the functions that need it raises.
+
+    plan = rpbh_plan(d, h=128, seed=0)                         # Sec. 4.4, Eq. (9)
+    cb_w, cb_a = lloydmax_codebook(4, d), lloydmax_codebook(4, d)   # Sec. 3.2, Eqs. (2)-(3)
+    w_codes, w_norm = quantize_weights_offline(plan, cb_w, W)  # Sec. 4.2, Eqs. (4)-(6)
+    x_codes, x_norm = rpbh_quantize_act(plan, cb_a, X)          # Sec. 4.3, Eqs. (7)-(8)
+    Y = orbit_qlinear(cb_a, x_codes, x_norm, cb_w, w_codes, w_norm)   # Y ~= X W^T
+"""
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liborbitquant.so")
+
+ORBIT_OK, ORBIT_EINVAL, ORBIT_EUNSUPPORTED, ORBIT_ENOMEM, ORBIT_EHIP, ORBIT_EINTERNAL = range(6)
+_STATUS_NAMES = {1: "EINVAL", 2: "EUNSUPPORTED", 3: "ENOMEM", 4: "EHIP", 5: "EINTERNAL"}
+
+# Every symbol the C header declares, with its ctypes signature.
+_c_void_p, _i64, _i32, _u64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
+SIGNATURES = {
+    "orbit_last_error": (ctypes.c_char_p, []),
+    "orbit_version": (ctypes.c_char_p, []),
+    "rpbh_plan": (ctypes.c_int, [_i64, _i32, _u64, ctypes.POINTER(_c_void_p)]),
+    "rpbh_plan_from_arrays": (ctypes.c_int, [_i64, _i32, _c_void_p, _c_void_p, ctypes.POINTER(_c_void_p)]),
+    "rpbh_plan_get": (ctypes.c_int, [_c_void_p, ctypes.POINTER(_i64), ctypes.POINTER(_i32), _c_void_p, _c_void_p]),
+    "rpbh_plan_destroy": (None, [_c_void_p]),
+    "lloydmax_codebook": (ctypes.c_int, [_i32, _i64, ctypes.POINTER(_c_void_p)]),
+    "lloydmax_codebook_get": (ctypes.c_int, [_c_void_p, ctypes.POINTER(_i32), ctypes.POINTER(_i64),
+                                             _c_void_p, _c_void_p, _c_void_p]),
+    "lloydmax_codebook_destroy": (None, [_c_void_p]),
+    "quantize_weights_offline": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i64,
+                                                ctypes.c_float, _c_void_p, _c_void_p, _c_void_p]),
+    "rpbh_quantize_act": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i64,
+                                         ctypes.c_float, _c_void_p, _c_void_p, _c_void_p]),
+    "orbit_qlinear": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
+                                     _c_void_p, _i64, _i64, _c_void_p, _i64, _c_void_p]),
+}
+
+_lib = None
+
+
+class OrbitError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn} failed with ORBIT_{_STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built (run paper_2607_02461_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_02461_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(handle, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _check(fn: str, status: int):
+    if status != ORBIT_OK:
+        raise OrbitError(fn, status, lib().orbit_last_error().decode())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+class Plan:
+    """Handle of an RPBH plan (perm + signs + block size) for one input dimension."""
+
+    def __init__(self, handle):
+        self._h = handle
+
+    @property
+    def handle(self):
+        return self._h
+
+    def _get(self):
+        d, h = _i64(), _i32()
+        _check("rpbh_plan_get", lib().rpbh_plan_get(self._h, ctypes.byref(d), ctypes.byref(h), None, None))
+        return d.value, h.value
+
+    @property
+    def d(self):
+        return self._get()[0]
+
+    @property
+    def h(self):
+        return self._get()[1]
+
+    def arrays(self):
+        """(perm int32 [d], sign int8 [d]) as numpy arrays."""
+        d = self.d
+        perm = np.empty(d, dtype=np.int32)
+        sign = np.empty(d, dtype=np.int8)
+        _check("rpbh_plan_get", lib().rpbh_plan_get(self._h, None, None, perm.ctypes.data, sign.ctypes.data))
+        return perm, sign
+
+    def __del__(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.rpbh_plan_destroy(self._h)
+            self._h = None
+
+
+class Codebook:
+    """Handle of a Lloyd-Max codebook C^(d,b)."""
+
+    def __init__(self, handle):
+        self._h = handle
+        b, d = _i32(), _i64()
+        _check("lloydmax_codebook_get", lib().lloydmax_codebook_get(handle, ctypes.byref(b), ctypes.byref(d),
+                                                                     None, None, None))
+        self.bits, self.d = b.value, d.value
+        n = 1 << self.bits
+        self.levels = np.empty(n, dtype=np.float64)
+        self.thresholds = np.empty(n - 1, dtype=np.float64)
+        self.lut_f16 = np.empty(n, dtype=np.uint16)
+        _check("lloydmax_codebook_get", lib().lloydmax_codebook_get(handle, None, None, self.levels.ctypes.data,
+                                                                     self.thresholds.ctypes.data,
+                                                                     self.lut_f16.ctypes.data))
+
+    @property
+    def handle(self):
+        return self._h
+
+    def __del__(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.lloydmax_codebook_destroy(self._h)
+            self._h = None
+
+
+def rpbh_plan(d: int, h: int = 128, seed: int = 0) -> Plan:
+    out = _c_void_p()
+    _check("rpbh_plan", lib().rpbh_plan(d, h, seed, ctypes.byref(out)))
+    return Plan(out)
+
+
+def rpbh_plan_from_arrays(d: int, h: int, perm, sign) -> Plan:
+    perm = np.ascontiguousarray(perm, dtype=np.int32)
+    sign = np.ascontiguousarray(sign, dtype=np.int8)
+    if perm.shape != (d,) or sign.shape != (d,):
+        raise ValueError("perm and sign must have d entries")
+    out = _c_void_p()
+    _check("rpbh_plan_from_arrays", lib().rpbh_plan_from_arrays(d, h, perm.ctypes.data, sign.ctypes.data,
+                                                                 ctypes.byref(out)))
+    return Plan(out)
+
+
+def lloydmax_codebook(bits: int, d: int) -> Codebook:
+    out = _c_void_p()
+    _check("lloydmax_codebook", lib().lloydmax_codebook(bits, d, ctypes.byref(out)))
+    return Codebook(out)
+
+
+def code_bytes(K: int, bits: int) -> int:
+    return K * bits // 8
+
+
+def _rows(t: torch.Tensor, name: str):
+    if t.dim() != 2 or t.dtype != torch.bfloat16 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a 2-D bf16 tensor with contiguous rows")
+    return t.shape[0], t.shape[1], t.stride(0)
+
+
+def quantize_weights_offline(plan: Plan, cb_w: Codebook, W: torch.Tensor, eps: float = 1e-10,
+                             codes: torch.Tensor = None, norms: torch.Tensor = None):
+    """Offline weight pass: returns (codes uint8 [N, K*b/8], r' bf16 [N])."""
+    N, K, ldw = _rows(W, "W")
+    if codes is None:
+        codes = torch.empty((N, code_bytes(K, cb_w.bits)), dtype=torch.uint8, device=W.device)
+    if norms is None:
+        norms = torch.empty((N,), dtype=torch.bfloat16, device=W.device)
+    _check("quantize_weights_offline", lib().quantize_weights_offline(
+        plan.handle, cb_w.handle, _ptr(W), N, K, ldw, eps, _ptr(codes), _ptr(norms), _stream(W)))
+    return codes, norms
+
+
+def rpbh_quantize_act(plan: Plan, cb_a: Codebook, X: torch.Tensor, eps: float = 1e-10,
+                      codes: torch.Tensor = None, norms: torch.Tensor = None):
+    """Online activation quantizer: returns (codes uint8 [M, K*b/8], s fp32 [M])."""
+    M, K, ldx = _rows(X, "X")
+    if codes is None:
+        codes = torch.empty((M, code_bytes(K, cb_a.bits)), dtype=torch.uint8, device=X.device)
+    if norms is None:
+        norms = torch.empty((M,), dtype=torch.float32, device=X.device)
+    _check("rpbh_quantize_act", lib().rpbh_quantize_act(
+        plan.handle, cb_a.handle, _ptr(X), M, K, ldx, eps, _ptr(codes), _ptr(norms), _stream(X)))
+    return codes, norms
+
+
+def orbit_qlinear(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor, cb_w: Codebook,
+                  w_codes: torch.Tensor, w_norm: torch.Tensor, out: torch.Tensor = None) -> torch.Tensor:
+    """Quantized layer on codes: Y fp32 [M, N] = diag(s) La[Xc] Lw[Wc]^T diag(r')."""
+    M, N = x_codes.shape[0], w_codes.shape[0]
+    K = cb_a.d
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=x_codes.device)
+    if out.dim() != 2 or out.stride(1) != 1 or out.dtype != torch.float32:
+        raise ValueError("out must be a 2-D fp32 tensor with contiguous rows")
+    _check("orbit_qlinear", lib().orbit_qlinear(
+        cb_a.handle, _ptr(x_codes), _ptr(x_norm), M, cb_w.handle, _ptr(w_codes), _ptr(w_norm), N, K,
+        _ptr(out), out.stride(0), _stream(x_codes)))
+    return out
+
+
+__all__ = ["rpbh_plan", "rpbh_plan_from_arrays", "lloydmax_codebook", "quantize_weights_offline",
+           "rpbh_quantize_act", "orbit_qlinear", "Plan", "Codebook", "OrbitError", "lib", "LIB_PATH",
+           "SIGNATURES", "code_bytes"]

@@ -1,0 +1,42 @@
+// Kernel parameter blocks and launchers shared by the device entry points and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace orbit {
+
+// Fused RPBH quantizer (activations: fp32 norms; weights: bf16 norms).
+struct QuantParams {
+    const uint16_t* X;     // bf16 [M][ldx]
+    int64_t ldx;           // elements
+    int64_t M;
+    const uint32_t* meta;  // [K]: (2*perm[j]) | sign bit << 31
+    uint8_t* codes;        // [M][K*bits/8]
+    void* norm;            // fp32 or bf16 [M]
+    int K, nb, R;          // input dim, K/128 blocks, rows staged per workgroup iteration
+    int ngroups;           // ceil(M / R)
+    float eps;
+    float thr[15];         // 2^bits - 1 ascending fp32 thresholds
+};
+
+int quant_rows_per_group(int K);
+size_t quant_smem_bytes(int K, int R);
+hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, int grid, hipStream_t stream);
+
+// LUT-decode GEMM: Y = diag(sx) La[Xc] (Lw[Wc])^T diag(rw).
+struct GemmParams {
+    const uint8_t* xc;     // [M][K*ba/8]
+    const float* xn;       // [M]
+    const uint8_t* wc;     // [N][K*bw/8]
+    const uint16_t* wn;    // bf16 [N]
+    float* Y;              // [M][ldy]
+    int64_t M, N, ldy;
+    int K;
+    uint16_t lut_a[16];    // fp16 levels (2^ba used)
+    uint16_t lut_w[16];    // fp16 levels (2^bw used)
+};
+
+hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, hipStream_t stream);
+
+}  // namespace orbit

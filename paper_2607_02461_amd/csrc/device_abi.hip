@@ -1,0 +1,179 @@
+// Device entry points of the C ABI: argument checks, per-device plan tables, kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "device.h"
+#include "internal.h"
+
+using namespace orbit;
+
+namespace {
+
+constexpr int kQuantH = 128;       // block size implemented by the fused quantizer
+constexpr int64_t kQuantMaxK = 16384;
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+orbit_status hip_fail(hipError_t e, const char* what) {
+    return fail(ORBIT_EHIP, "%s: %s (%s)", what, hipGetErrorString(e), hipGetErrorName(e));
+}
+
+struct DeviceInfo {
+    int cus = 0;
+};
+DeviceInfo g_dev[kMaxDevices];
+std::mutex g_dev_mu;
+
+orbit_status current_device(int* dev, DeviceInfo* info) {
+    hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (*dev < 0 || *dev >= kMaxDevices) return fail(ORBIT_EUNSUPPORTED, "device ordinal %d out of range", *dev);
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    if (g_dev[*dev].cus == 0) {
+        int cus = 0;
+        e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, *dev);
+        if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+        g_dev[*dev].cus = cus > 0 ? cus : 1;
+    }
+    *info = g_dev[*dev];
+    return ORBIT_OK;
+}
+
+// The plan's gather/sign table on device `dev`, uploaded on first use.
+orbit_status plan_meta(orbit_plan p, int dev, const uint32_t** out) {
+    std::lock_guard<std::mutex> lk(p->mu);
+    if (!p->dev_meta[dev]) {
+        std::vector<uint32_t> meta((size_t)p->d);
+        for (int64_t j = 0; j < p->d; ++j)
+            meta[j] = ((uint32_t)p->perm[j] * 2u) | (p->sign[j] < 0 ? 0x80000000u : 0u);
+        void* d = nullptr;
+        hipError_t e = hipMalloc(&d, meta.size() * sizeof(uint32_t));
+        if (e != hipSuccess) return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "plan upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
+        e = hipMemcpy(d, meta.data(), meta.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            hipFree(d);
+            return hip_fail(e, "plan upload: hipMemcpy");
+        }
+        p->dev_meta[dev] = (uint32_t*)d;
+    }
+    *out = p->dev_meta[dev];
+    return ORBIT_OK;
+}
+
+orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, const uint16_t* X, int64_t M, int64_t K,
+                           int64_t ldx, float eps, uint8_t* codes, void* norm, bool norm_bf16, void* stream) {
+    clear_error();
+    if (!p || !cb) return fail(ORBIT_EINVAL, "%s: plan or codebook is NULL", who);
+    if (M < 0) return fail(ORBIT_EINVAL, "%s: negative row count %lld", who, (long long)M);
+    if (K != p->d || K != cb->d)
+        return fail(ORBIT_EINVAL, "%s: K=%lld but plan.d=%lld and codebook.d=%lld", who, (long long)K, (long long)p->d,
+                    (long long)cb->d);
+    if (!(eps >= 0.0f) || !std::isfinite(eps)) return fail(ORBIT_EINVAL, "%s: eps must be finite and >= 0", who);
+    if (ldx < K || ldx % 8 != 0) return fail(ORBIT_EINVAL, "%s: ld=%lld must be >= K and a multiple of 8", who, (long long)ldx);
+    if (p->h != kQuantH) return fail(ORBIT_EUNSUPPORTED, "%s: block size h=%d not implemented (h=128 is)", who, p->h);
+    if (cb->bits < 2 || cb->bits > 4) return fail(ORBIT_EUNSUPPORTED, "%s: %d-bit codes not implemented (2..4 are)", who, cb->bits);
+    if (K > kQuantMaxK) return fail(ORBIT_EUNSUPPORTED, "%s: K=%lld above %lld", who, (long long)K, (long long)kQuantMaxK);
+    if (M == 0) return ORBIT_OK;
+    if (!X || !codes || !norm) return fail(ORBIT_EINVAL, "%s: null device pointer", who);
+    if (!aligned(X, 16) || !aligned(codes, 16) || !aligned(norm, norm_bf16 ? 2 : 4))
+        return fail(ORBIT_EINVAL, "%s: misaligned pointer (input and codes need 16 bytes)", who);
+    int dev;
+    DeviceInfo info;
+    orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    const uint32_t* meta = nullptr;
+    st = plan_meta(p, dev, &meta);
+    if (st != ORBIT_OK) return st;
+
+    QuantParams q{};
+    q.X = X;
+    q.ldx = ldx;
+    q.M = M;
+    q.meta = meta;
+    q.codes = codes;
+    q.norm = norm;
+    q.K = (int)K;
+    q.nb = (int)(K / kQuantH);
+    q.R = quant_rows_per_group((int)K);
+    q.ngroups = (int)((M + q.R - 1) / q.R);
+    q.eps = eps;
+    const int nthr = (1 << cb->bits) - 1;
+    for (int j = 0; j < 15; ++j) q.thr[j] = j < nthr ? (float)cb->thresholds[j] : INFINITY;
+    const int grid = (int)std::min<int64_t>(q.ngroups, (int64_t)info.cus * 4);
+    hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, grid, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, who);
+    return ORBIT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void rpbh_plan_destroy(orbit_plan p) {
+    if (!p) return;
+    for (int dev = 0; dev < kMaxDevices; ++dev) {
+        if (p->dev_meta[dev]) {
+            int cur = 0;
+            hipGetDevice(&cur);
+            hipSetDevice(dev);
+            hipFree(p->dev_meta[dev]);
+            hipSetDevice(cur);
+        }
+    }
+    delete p;
+}
+
+orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const uint16_t* W, int64_t N, int64_t K,
+                                      int64_t ldw, float eps, uint8_t* w_codes, uint16_t* w_norm, void* stream) {
+    return quantize_rows("quantize_weights_offline", p, cb_w, W, N, K, ldw, eps, w_codes, w_norm, true, stream);
+}
+
+orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t* X, int64_t M, int64_t K, int64_t ldx,
+                               float eps, uint8_t* x_codes, float* x_norm, void* stream) {
+    return quantize_rows("rpbh_quantize_act", p, cb_a, X, M, K, ldx, eps, x_codes, x_norm, false, stream);
+}
+
+orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                           orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N, int64_t K,
+                           float* Y, int64_t ldy, void* stream) {
+    clear_error();
+    if (!cb_a || !cb_w) return fail(ORBIT_EINVAL, "orbit_qlinear: codebook is NULL");
+    if (M < 0 || N < 0) return fail(ORBIT_EINVAL, "orbit_qlinear: negative M or N");
+    if (K != cb_a->d || K != cb_w->d)
+        return fail(ORBIT_EINVAL, "orbit_qlinear: K=%lld but codebooks have d=%lld and d=%lld", (long long)K,
+                    (long long)cb_a->d, (long long)cb_w->d);
+    if (ldy < N) return fail(ORBIT_EINVAL, "orbit_qlinear: ldy=%lld < N=%lld", (long long)ldy, (long long)N);
+    if (cb_a->bits < 2 || cb_a->bits > 4 || cb_w->bits < 2 || cb_w->bits > 4)
+        return fail(ORBIT_EUNSUPPORTED, "orbit_qlinear: bit-widths (%d, %d) not implemented (2..4 are)", cb_a->bits, cb_w->bits);
+    if (K % 64 != 0 || K > (int64_t)1 << 30) return fail(ORBIT_EUNSUPPORTED, "orbit_qlinear: K=%lld must be a multiple of 64", (long long)K);
+    if (M == 0 || N == 0) return ORBIT_OK;
+    if (!x_codes || !x_norm || !w_codes || !w_norm || !Y) return fail(ORBIT_EINVAL, "orbit_qlinear: null device pointer");
+    if (!aligned(x_codes, 16) || !aligned(w_codes, 16) || !aligned(x_norm, 4) || !aligned(w_norm, 2) || !aligned(Y, 4))
+        return fail(ORBIT_EINVAL, "orbit_qlinear: misaligned pointer (codes need 16 bytes)");
+    int dev;
+    DeviceInfo info;
+    orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    GemmParams g{};
+    g.xc = x_codes;
+    g.xn = x_norm;
+    g.wc = w_codes;
+    g.wn = w_norm;
+    g.Y = Y;
+    g.M = M;
+    g.N = N;
+    g.ldy = ldy;
+    g.K = (int)K;
+    for (int j = 0; j < 16; ++j) {
+        g.lut_a[j] = j < (1 << cb_a->bits) ? cb_a->lut_f16[j] : 0;
+        g.lut_w[j] = j < (1 << cb_w->bits) ? cb_w->lut_f16[j] : 0;
+    }
+    hipError_t e = launch_lut_gemm(g, cb_a->bits, cb_w->bits, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "orbit_qlinear");
+    return ORBIT_OK;
+}
+
+}  // extern "C"

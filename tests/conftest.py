@@ -23,3 +23,14 @@ def read_golden(name):
             if line:
                 rows.append([c.strip() for c in line.split("|")])
     return rows
+
+
+def _ensure_built():
+    """Tests use the in-tree library as built; they build it only if nothing is there."""
+    lib = os.path.join(ROOT, "paper_2607_02461_amd", "liborbitquant.so")
+    if not os.path.exists(lib):
+        from paper_2607_02461_amd.build import build
+        build()
+
+
+_ensure_built()

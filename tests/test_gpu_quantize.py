@@ -1,0 +1,126 @@
+"""GPU parity of the fused RPBH quantizer (activations and the offline weight pass) against
+the fp64 oracle: codes bit-exact wherever the normalized rotated value lies more than 1e-5
+from a decision threshold (near-ties are counted and logged), fp32 norms within 1e-5
+relative, BF16 weight norms within one BF16 ulp."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_02461_amd as oq
+from paper_2607_02461_amd import workloads
+from tests.gpu_util import compare_quantizer, quantize_gpu, log_stats
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _randn_bf16(M, K, seed, scale=1.0):
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    return (torch.randn((M, K), generator=g, device=DEV) * scale).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("K,M", [(128, 1), (384, 3), (1024, 64), (3072, 257), (128, 1000), (16384, 5),
+                                 (5120, 130), (13824, 3)])
+@pytest.mark.parametrize("bits", [2, 3, 4])
+@pytest.mark.parametrize("weights", [False, True])
+def test_small_shapes(K, M, bits, weights):
+    X = _randn_bf16(M, K, seed=K * 7 + M)
+    compare_quantizer(f"small K={K} M={M}", X, bits, seed=K % 5, weights=weights)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_c1_activations_full(seed, bits):
+    X, _ = workloads.c1_inputs(device=DEV)
+    compare_quantizer(f"c1 act seed={seed}", X, bits, seed=seed)
+
+
+def test_c1_weights_full():
+    _, W = workloads.c1_inputs(device=DEV)
+    compare_quantizer("c1 weights", W, 4, seed=0, weights=True)
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_c3_activations_full(bits):
+    Xq, _, _, _ = workloads.c3_inputs(device=DEV)
+    compare_quantizer(f"c3 qkv act A{bits}", Xq, bits, seed=0)
+
+
+def test_c3_weights_outlier_rows():
+    _, _, Wq, _ = workloads.c3_inputs(device=DEV)
+    compare_quantizer("c3 qkv weights W2", Wq, 2, seed=0, weights=True)
+
+
+def test_c4_down_sampled_rows():
+    # the full video-DiT down-projection input in the launch configuration the benchmark times
+    fr, tpf, txt = 21, 30 * 52, 512
+    X = workloads.video_acts(fr * tpf, txt, 13824, 4, fr, workloads.C4.data_seed, 1, device=DEV)
+    rows = np.sort(np.random.default_rng(44).choice(X.shape[0], 4096, replace=False))
+    rows[-1] = X.shape[0] - 1                     # include the ragged tail
+    compare_quantizer("c4 down act sampled", X, 4, seed=0, rows=rows)
+
+
+def test_c4_up_weights_sampled_rows():
+    W = workloads.gaussian_weights(13824, 5120, 0.015, workloads.C4.data_seed, 0, device=DEV)
+    rows = np.sort(np.random.default_rng(45).choice(W.shape[0], 2048, replace=False))
+    compare_quantizer("c4 up weights sampled", W, 4, seed=0, weights=True, rows=rows)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_zero_rows(bits):
+    X = _randn_bf16(9, 256, seed=3)
+    X[2] = 0
+    X[7] = 0
+    codes, norms = quantize_gpu(X, bits)
+    gc = oracle.unpack_codes(codes.cpu().numpy(), bits, 256)
+    assert norms[2].item() == 0.0 and norms[7].item() == 0.0
+    assert np.all(gc[2] == 1 << (bits - 1)) and np.all(gc[7] == 1 << (bits - 1))
+    cw, nw = quantize_gpu(X, bits, weights=True)
+    assert nw[2].item() == 0.0
+
+
+@pytest.mark.parametrize("bits", [2, 4])
+def test_power_of_two_scaling_is_exact(bits):
+    # codes depend only on the direction; the norm scales exactly (eps = 0 so nothing is added)
+    X = _randn_bf16(33, 3072, seed=5)
+    c0, n0 = quantize_gpu(X, bits, eps=0.0)
+    for k in (-6, 5):
+        ck, nk = quantize_gpu((X.float() * 2.0 ** k).to(torch.bfloat16), bits, eps=0.0)
+        assert torch.equal(ck, c0)
+        assert torch.equal(nk, n0 * 2.0 ** k)
+
+
+def test_deterministic():
+    X = _randn_bf16(300, 5120, seed=9)
+    a = quantize_gpu(X, 4)
+    b = quantize_gpu(X, 4)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
+
+
+def test_plan_from_caller_arrays():
+    K = 3072
+    g = torch.Generator()
+    g.manual_seed(77)
+    perm = torch.randperm(K, generator=g).numpy()
+    sign = np.where(torch.rand(K, generator=g).numpy() < 0.5, -1, 1)
+    plan = oq.rpbh_plan_from_arrays(K, 128, perm, sign)
+    oplan = oracle.Plan(d=K, h=128, perm=perm.astype(np.int64), sign=sign.astype(np.float64))
+    X, _ = workloads.c1_inputs(device=DEV)
+    compare_quantizer("c1 act caller plan", X, 4, plan=plan, oplan=oplan)
+
+
+def test_strided_rows():
+    base = _randn_bf16(40, 3072 + 64, seed=11)
+    X = base[:, 32:32 + 3072]            # ldx = 3136, rows start 64 bytes in
+    assert X.stride(0) == 3136
+    compare_quantizer("strided rows", X, 4, seed=1)
+
+
+def test_zero_row_count_is_noop():
+    X = torch.empty((0, 256), dtype=torch.bfloat16, device=DEV)
+    codes, norms = quantize_gpu(X, 4)
+    assert codes.shape == (0, 128) and norms.shape == (0,)

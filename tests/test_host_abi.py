@@ -1,0 +1,159 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, its host-side
+plan and codebook match the oracle, and device calls reject bad arguments before any
+launch (no GPU work is started by these tests)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_02461_amd as oq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "orbitquant.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(\w+)\s*\(", src, flags=re.M)) - {"if"})
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = oq.lib()
+    names = declared_functions()
+    assert len(names) >= 12
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(oq.SIGNATURES), "binding signatures must cover the header exactly"
+    assert lib.orbit_version().decode().startswith("orbitquant")
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+@pytest.mark.parametrize("d", [16, 64, 3072, 5120, 12288, 13824])
+def test_codebook_matches_oracle(bits, d):
+    cb = oq.lloydmax_codebook(bits, d)
+    ref = oracle.lloydmax_codebook(bits, d)
+    assert cb.bits == bits and cb.d == d
+    assert np.max(np.abs(cb.levels - ref.levels) / np.abs(ref.levels)) < 1e-12
+    assert np.max(np.abs(cb.thresholds - ref.thresholds)) < 1e-12 * np.max(np.abs(ref.levels))
+    # exact antisymmetry, middle threshold exactly zero
+    assert np.array_equal(cb.levels, -cb.levels[::-1])
+    assert cb.thresholds[(1 << bits) // 2 - 1] == 0.0
+    # the fp16 image equals round-to-nearest-even of the oracle's levels
+    want = ref.levels.astype(np.float16).view(np.uint16)
+    assert np.array_equal(cb.lut_f16, want)
+
+
+def test_codebook_d3_uniform_and_large_d():
+    cb = oq.lloydmax_codebook(3, 3)
+    assert np.max(np.abs(cb.levels - (-1 + (2 * np.arange(8) + 1) / 8))) < 1e-13
+    big = oq.lloydmax_codebook(2, 10 ** 6)
+    assert np.max(np.abs(big.levels[2:] * 1000 - [0.4528, 1.510])) < 6e-4
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 12345, 2 ** 63 + 7])
+@pytest.mark.parametrize("d,h", [(3072, 128), (5120, 128), (13824, 128), (24, 8), (1920, 0)])
+def test_plan_matches_oracle(seed, d, h):
+    p = oq.rpbh_plan(d, h, seed)
+    perm, sign = p.arrays()
+    hh = h if h else (d & -d)
+    ref = oracle.rpbh_plan(d, hh, seed)
+    assert p.d == d and p.h == hh
+    assert np.array_equal(perm, ref.perm)
+    assert np.array_equal(sign.astype(np.float64), ref.sign)
+
+
+def test_plan_block_size_rule():
+    # Sec. 4.4: h is the largest power of two dividing d
+    for d, h in ((3072, 1024), (5120, 1024), (12288, 4096), (13824, 512), (1920, 128)):
+        assert oq.rpbh_plan(d, 0, 0).h == h
+
+
+def test_plan_from_arrays_roundtrip_and_validation():
+    perm = np.random.default_rng(0).permutation(256).astype(np.int32)
+    sign = np.where(np.random.default_rng(1).random(256) < 0.5, -1, 1).astype(np.int8)
+    p = oq.rpbh_plan_from_arrays(256, 128, perm, sign)
+    got_perm, got_sign = p.arrays()
+    assert np.array_equal(got_perm, perm) and np.array_equal(got_sign, sign)
+    bad = perm.copy()
+    bad[3] = bad[4]
+    with pytest.raises(oq.OrbitError) as e:
+        oq.rpbh_plan_from_arrays(256, 128, bad, sign)
+    assert e.value.status == oq.ORBIT_EINVAL
+    bad_sign = sign.copy()
+    bad_sign[0] = 0
+    with pytest.raises(oq.OrbitError):
+        oq.rpbh_plan_from_arrays(256, 128, perm, bad_sign)
+
+
+@pytest.mark.parametrize("d,h", [(100, 3), (96, 64), (0, 1), (-5, 1)])
+def test_plan_rejects_bad_arguments(d, h):
+    with pytest.raises(oq.OrbitError) as e:
+        oq.rpbh_plan(d, h, 0)
+    assert e.value.status == oq.ORBIT_EINVAL
+
+
+@pytest.mark.parametrize("bits,d", [(0, 64), (7, 64), (2, 2), (3, 0)])
+def test_codebook_rejects_bad_arguments(bits, d):
+    with pytest.raises(oq.OrbitError) as e:
+        oq.lloydmax_codebook(bits, d)
+    assert e.value.status == oq.ORBIT_EINVAL
+
+
+def _status(fn, *args):
+    st = fn(*args)
+    return st, oq.lib().orbit_last_error().decode()
+
+
+def test_device_calls_validate_before_launch():
+    lib = oq.lib()
+    p = oq.rpbh_plan(256, 128, 0)
+    p_h64 = oq.rpbh_plan(256, 64, 0)
+    cb4 = oq.lloydmax_codebook(4, 256)
+    cb1 = oq.lloydmax_codebook(1, 256)
+    cb_other = oq.lloydmax_codebook(4, 512)
+    null = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)   # never dereferenced: every case fails validation first
+    # K mismatch
+    st, msg = _status(lib.rpbh_quantize_act, p.handle, cb_other.handle, fake, 4, 256, 256, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EINVAL and "K=" in msg
+    # unsupported block size and bit-width
+    st, _ = _status(lib.rpbh_quantize_act, p_h64.handle, cb4.handle, fake, 4, 256, 256, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EUNSUPPORTED
+    st, _ = _status(lib.rpbh_quantize_act, p.handle, cb1.handle, fake, 4, 256, 256, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EUNSUPPORTED
+    # bad stride, negative rows, bad eps, null pointers, misalignment
+    st, _ = _status(lib.rpbh_quantize_act, p.handle, cb4.handle, fake, 4, 256, 100, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EINVAL
+    st, _ = _status(lib.rpbh_quantize_act, p.handle, cb4.handle, fake, -1, 256, 256, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EINVAL
+    st, _ = _status(lib.rpbh_quantize_act, p.handle, cb4.handle, fake, 4, 256, 256, float("nan"), fake, fake, null)
+    assert st == oq.ORBIT_EINVAL
+    st, _ = _status(lib.rpbh_quantize_act, p.handle, cb4.handle, null, 4, 256, 256, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EINVAL
+    st, _ = _status(lib.quantize_weights_offline, p.handle, cb4.handle, ctypes.c_void_p((1 << 20) + 2), 4, 256,
+                    256, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EINVAL
+    st, _ = _status(lib.rpbh_quantize_act, None, cb4.handle, fake, 4, 256, 256, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EINVAL
+    # zero rows is a successful no-op (no device touched)
+    st, _ = _status(lib.rpbh_quantize_act, p.handle, cb4.handle, null, 0, 256, 256, 1e-10, null, null, null)
+    assert st == oq.ORBIT_OK
+    st, _ = _status(lib.quantize_weights_offline, p.handle, cb4.handle, null, 0, 256, 256, 1e-10, null, null, null)
+    assert st == oq.ORBIT_OK
+    # qlinear
+    st, _ = _status(lib.orbit_qlinear, cb4.handle, fake, fake, 4, cb_other.handle, fake, fake, 4, 256, fake, 4, null)
+    assert st == oq.ORBIT_EINVAL
+    st, _ = _status(lib.orbit_qlinear, cb4.handle, fake, fake, 4, cb4.handle, fake, fake, 8, 256, fake, 4, null)
+    assert st == oq.ORBIT_EINVAL   # ldy < N
+    st, _ = _status(lib.orbit_qlinear, cb1.handle, fake, fake, 4, cb4.handle, fake, fake, 4, 256, fake, 4, null)
+    assert st == oq.ORBIT_EUNSUPPORTED
+    st, _ = _status(lib.orbit_qlinear, cb4.handle, null, null, 0, cb4.handle, null, null, 4, 256, null, 4, null)
+    assert st == oq.ORBIT_OK
+    st, _ = _status(lib.orbit_qlinear, cb4.handle, null, null, 4, cb4.handle, null, null, 0, 256, null, 0, null)
+    assert st == oq.ORBIT_OK
+    assert lib.orbit_last_error().decode() == ""

@@ -160,3 +160,11 @@ def test_end_to_end_error_band(bw, ba, lo, hi):
     ref = oracle.qlinear_dense_reference(X, W)
     err = np.linalg.norm(Y - ref) / np.linalg.norm(ref)
     assert lo < err < hi, err
+
+
+def test_near_tie_mask_matches_bruteforce_distance():
+    cb = _cb(4, 3072)
+    u = np.concatenate([np.random.default_rng(7).normal(size=4000) / math.sqrt(3072),
+                        cb.thresholds + 3e-6, cb.thresholds - 2e-5])
+    brute = np.min(np.abs(u[:, None] - cb.thresholds[None, :]), axis=1) <= 1e-5
+    assert np.array_equal(oracle.near_tie_mask(u, cb.thresholds, 1e-5), brute)
