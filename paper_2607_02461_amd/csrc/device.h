@@ -11,17 +11,21 @@ struct QuantParams {
     const uint16_t* X;     // bf16 [M][ldx]
     int64_t ldx;           // elements
     int64_t M;
-    const uint32_t* meta;  // [K]: (2*perm[j]) | sign bit << 31
+    const uint32_t* meta;  // [K]: 2*perm[j], the byte offset of the gathered element in a staged row
+    const uint32_t* smask; // [K/2]: bf16 sign bits to XOR into staged element pairs (source positions)
     uint8_t* codes;        // [M][K*bits/8]
     void* norm;            // fp32 or bf16 [M]
     int K, nb, R;          // input dim, K/128 blocks, rows staged per workgroup iteration
     int ngroups;           // ceil(M / R)
     float eps;
-    float thr[15];         // 2^bits - 1 ascending fp32 thresholds
+    const uint32_t* enc;   // encoder table: ncell pairs (threshold in cell units as fp32 bits, base code)
+    int ncell;
+    float enc_inv_w;       // cells per unit of the normalized coordinate
+    float enc_center;      // cell coordinate of u = 0
 };
 
 int quant_rows_per_group(int K);
-size_t quant_smem_bytes(int K, int R);
+size_t quant_smem_bytes(int K, int R, int ncell);
 hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, int grid, hipStream_t stream);
 
 // LUT-decode GEMM: Y = diag(sx) La[Xc] (Lw[Wc])^T diag(rw).

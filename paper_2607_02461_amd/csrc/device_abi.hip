@@ -14,6 +14,7 @@ namespace {
 
 constexpr int kQuantH = 128;       // block size implemented by the fused quantizer
 constexpr int64_t kQuantMaxK = 16384;
+constexpr int kQuantMaxCells = 2048;  // encoder table cells (LDS budget)
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
@@ -42,24 +43,53 @@ orbit_status current_device(int* dev, DeviceInfo* info) {
     return ORBIT_OK;
 }
 
-// The plan's gather/sign table on device `dev`, uploaded on first use.
+// The plan's tables on device `dev`, uploaded on first use: K gather offsets (2*perm[j], the
+// byte offset of the element that moves to position j) followed by K/2 sign masks over source
+// positions (bit 15 / bit 31 of word i carry the sign applied to source elements 2i / 2i+1, i.e.
+// the sign of the position each of them moves to), repeated once per row slot of a staged group.
 orbit_status plan_meta(orbit_plan p, int dev, const uint32_t** out) {
     std::lock_guard<std::mutex> lk(p->mu);
     if (!p->dev_meta[dev]) {
-        std::vector<uint32_t> meta((size_t)p->d);
-        for (int64_t j = 0; j < p->d; ++j)
-            meta[j] = ((uint32_t)p->perm[j] * 2u) | (p->sign[j] < 0 ? 0x80000000u : 0u);
-        void* d = nullptr;
-        hipError_t e = hipMalloc(&d, meta.size() * sizeof(uint32_t));
+        const int64_t d = p->d;
+        const int64_t reps = d % 2 == 0 && d <= kQuantMaxK ? quant_rows_per_group((int)d) : 1;
+        std::vector<uint32_t> meta((size_t)(d + reps * ((d + 1) / 2)), 0u);
+        for (int64_t j = 0; j < d; ++j) {
+            const uint32_t src = (uint32_t)p->perm[j];
+            meta[j] = src * 2u;
+            if (p->sign[j] < 0) meta[d + src / 2] |= (src & 1u) ? 0x80000000u : 0x8000u;
+        }
+        for (int64_t r = 1; r < reps; ++r)
+            std::memcpy(&meta[d + r * (d / 2)], &meta[d], sizeof(uint32_t) * (d / 2));
+        void* dp = nullptr;
+        hipError_t e = hipMalloc(&dp, meta.size() * sizeof(uint32_t));
         if (e != hipSuccess) return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "plan upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
-        e = hipMemcpy(d, meta.data(), meta.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
+        e = hipMemcpy(dp, meta.data(), meta.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
         if (e != hipSuccess) {
-            hipFree(d);
+            (void)hipFree(dp);
             return hip_fail(e, "plan upload: hipMemcpy");
         }
-        p->dev_meta[dev] = (uint32_t*)d;
+        p->dev_meta[dev] = (uint32_t*)dp;
     }
     *out = p->dev_meta[dev];
+    return ORBIT_OK;
+}
+
+// The codebook's encoder table on device `dev`, uploaded on first use.
+orbit_status codebook_enc(orbit_codebook c, int dev, const uint32_t** out) {
+    std::lock_guard<std::mutex> lk(c->mu);
+    if (!c->dev_enc[dev]) {
+        const size_t bytes = c->enc.entries.size() * sizeof(uint32_t);
+        void* d = nullptr;
+        hipError_t e = hipMalloc(&d, bytes);
+        if (e != hipSuccess) return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "codebook upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
+        e = hipMemcpy(d, c->enc.entries.data(), bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            (void)hipFree(d);
+            return hip_fail(e, "codebook upload: hipMemcpy");
+        }
+        c->dev_enc[dev] = (uint32_t*)d;
+    }
+    *out = c->dev_enc[dev];
     return ORBIT_OK;
 }
 
@@ -76,6 +106,8 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     if (p->h != kQuantH) return fail(ORBIT_EUNSUPPORTED, "%s: block size h=%d not implemented (h=128 is)", who, p->h);
     if (cb->bits < 2 || cb->bits > 4) return fail(ORBIT_EUNSUPPORTED, "%s: %d-bit codes not implemented (2..4 are)", who, cb->bits);
     if (K > kQuantMaxK) return fail(ORBIT_EUNSUPPORTED, "%s: K=%lld above %lld", who, (long long)K, (long long)kQuantMaxK);
+    if ((int64_t)quant_rows_per_group((int)K) * ldx * 2 >= ((int64_t)1 << 31))
+        return fail(ORBIT_EUNSUPPORTED, "%s: row stride %lld too large", who, (long long)ldx);
     if (M == 0) return ORBIT_OK;
     if (!X || !codes || !norm) return fail(ORBIT_EINVAL, "%s: null device pointer", who);
     if (!aligned(X, 16) || !aligned(codes, 16) || !aligned(norm, norm_bf16 ? 2 : 4))
@@ -87,12 +119,18 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     const uint32_t* meta = nullptr;
     st = plan_meta(p, dev, &meta);
     if (st != ORBIT_OK) return st;
+    const uint32_t* enc = nullptr;
+    st = codebook_enc(cb, dev, &enc);
+    if (st != ORBIT_OK) return st;
+    if (cb->enc.ncell > kQuantMaxCells)
+        return fail(ORBIT_EUNSUPPORTED, "%s: encoder table of %d cells exceeds %d", who, cb->enc.ncell, kQuantMaxCells);
 
     QuantParams q{};
     q.X = X;
     q.ldx = ldx;
     q.M = M;
     q.meta = meta;
+    q.smask = meta + K;
     q.codes = codes;
     q.norm = norm;
     q.K = (int)K;
@@ -100,12 +138,30 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     q.R = quant_rows_per_group((int)K);
     q.ngroups = (int)((M + q.R - 1) / q.R);
     q.eps = eps;
-    const int nthr = (1 << cb->bits) - 1;
-    for (int j = 0; j < 15; ++j) q.thr[j] = j < nthr ? (float)cb->thresholds[j] : INFINITY;
-    const int grid = (int)std::min<int64_t>(q.ngroups, (int64_t)info.cus * 4);
+    q.enc = enc;
+    q.ncell = cb->enc.ncell;
+    q.enc_inv_w = cb->enc.inv_w;
+    q.enc_center = cb->enc.center;
+    // two workgroups fit a compute unit (LDS: double row buffer + encoder table)
+    const int grid = (int)std::min<int64_t>(q.ngroups, (int64_t)info.cus * 2);
     hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, grid, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, who);
     return ORBIT_OK;
+}
+
+// Frees a handle's per-device tables (each on its own device).
+template <typename T>
+void free_per_device(T* (&ptrs)[kMaxDevices]) {
+    for (int dev = 0; dev < kMaxDevices; ++dev) {
+        if (ptrs[dev]) {
+            int cur = 0;
+            (void)hipGetDevice(&cur);
+            (void)hipSetDevice(dev);
+            (void)hipFree(ptrs[dev]);
+            (void)hipSetDevice(cur);
+            ptrs[dev] = nullptr;
+        }
+    }
 }
 
 }  // namespace
@@ -114,16 +170,14 @@ extern "C" {
 
 void rpbh_plan_destroy(orbit_plan p) {
     if (!p) return;
-    for (int dev = 0; dev < kMaxDevices; ++dev) {
-        if (p->dev_meta[dev]) {
-            int cur = 0;
-            hipGetDevice(&cur);
-            hipSetDevice(dev);
-            hipFree(p->dev_meta[dev]);
-            hipSetDevice(cur);
-        }
-    }
+    free_per_device(p->dev_meta);
     delete p;
+}
+
+void lloydmax_codebook_destroy(orbit_codebook c) {
+    if (!c) return;
+    free_per_device(c->dev_enc);
+    delete c;
 }
 
 orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const uint16_t* W, int64_t N, int64_t K,

@@ -255,6 +255,31 @@ bool lloyd_max_positive_half(int64_t d, int bits, std::vector<double>& p_out) {
 }
 
 }  // namespace
+
+void build_enc_table(orbit_codebook_s* c) {
+    const std::vector<double>& tau = c->thresholds;
+    double min_gap = 2.0 * kEncRange;
+    for (size_t j = 1; j < tau.size(); ++j) min_gap = std::min(min_gap, tau[j] - tau[j - 1]);
+    const double w = 0.9 * min_gap;
+    const int ncell = (int)std::ceil(2.0 * kEncRange / w) + 2;
+    EncTable& e = c->enc;
+    e.inv_w = (float)(1.0 / w);
+    e.center = (float)(kEncRange / w);
+    e.ncell = ncell;
+    e.entries.assign(2 * (size_t)ncell, 0u);
+    size_t j = 0;  // thresholds below the current cell start
+    for (int cell = 0; cell < ncell; ++cell) {
+        const double lo = cell * w - kEncRange, hi = (cell + 1) * w - kEncRange;
+        while (j < tau.size() && tau[j] <= lo) ++j;
+        float tt = INFINITY;
+        if (j < tau.size() && tau[j] < hi) tt = (float)((tau[j] + kEncRange) / w);
+        uint32_t bits;
+        std::memcpy(&bits, &tt, 4);
+        e.entries[2 * cell] = bits;
+        e.entries[2 * cell + 1] = (uint32_t)j;
+    }
+}
+
 }  // namespace orbit
 
 using namespace orbit;
@@ -357,6 +382,7 @@ orbit_status lloydmax_codebook(int32_t bits, int64_t d, orbit_codebook* out) {
     }
     c->thresholds.resize(n - 1);
     for (int j = 0; j + 1 < n; ++j) c->thresholds[j] = 0.5 * (c->levels[j] + c->levels[j + 1]);
+    build_enc_table(c);
     c->lut_f16.resize(n);
     for (int j = 0; j < n; ++j) {
         _Float16 hv = (_Float16)c->levels[j];
@@ -380,7 +406,5 @@ orbit_status lloydmax_codebook_get(orbit_codebook c, int32_t* bits, int64_t* d, 
     if (lut_f16) std::memcpy(lut_f16, c->lut_f16.data(), n * sizeof(uint16_t));
     return ORBIT_OK;
 }
-
-void lloydmax_codebook_destroy(orbit_codebook c) { delete c; }
 
 }  // extern "C"

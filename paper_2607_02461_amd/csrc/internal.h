@@ -25,10 +25,21 @@ struct orbit_plan_s {
     int32_t h = 0;
     std::vector<int32_t> perm;  // y_j = x[perm[j]]
     std::vector<int8_t> sign;   // multiplies post-permutation coordinate j
-    // Per-device table for the quantizer: meta[j] = (2*perm[j]) | (sign[j] < 0 ? 1u << 31 : 0),
-    // i.e. the byte offset of the gathered bf16 element inside a staged row plus the sign bit.
+    // Per-device tables for the quantizer (gather offsets and sign masks), see plan_meta().
     std::mutex mu;
     uint32_t* dev_meta[orbit::kMaxDevices] = {};
+};
+
+// Encoder lookup table over the normalized coordinate u in [-kEncRange, kEncRange]: cell c covers
+// u in [c*w - kEncRange, (c+1)*w - kEncRange) with w below the smallest threshold spacing, so a cell
+// holds at most one threshold.  In cell coordinates t = (u + kEncRange) / w, the code of t in cell c
+// is base[c] + (t >= tthr[c]), with tthr = +inf for cells without a threshold.
+constexpr double kEncRange = 1.001;  // |u| <= 1 up to rounding
+struct EncTable {
+    float inv_w = 0.f;   // 1 / w
+    float center = 0.f;  // kEncRange / w
+    int32_t ncell = 0;
+    std::vector<uint32_t> entries;  // ncell pairs: (bits of tthr as fp32, base code)
 };
 
 // C^(d,b): ascending levels, midpoint thresholds, fp16 image of the levels.
@@ -38,4 +49,11 @@ struct orbit_codebook_s {
     std::vector<double> levels;
     std::vector<double> thresholds;
     std::vector<uint16_t> lut_f16;
+    EncTable enc;
+    std::mutex mu;
+    uint32_t* dev_enc[orbit::kMaxDevices] = {};
 };
+
+namespace orbit {
+void build_enc_table(orbit_codebook_s* c);
+}

@@ -3,19 +3,33 @@
 // One kernel serves the online activation quantizer (Sec. 4.3, Eqs. (7)-(8)) and the offline
 // weight pass (Sec. 4.2, Eqs. (4)-(6)); they differ only in the type of the stored norm.
 //
-// Work mapping (h = 128): a workgroup owns R rows at a time.  Each row is staged in LDS as raw
-// bf16 with 16-byte coalesced loads.  Every 128-block of a row belongs to one quad of lanes;
-// lane q of the quad holds the 32 consecutive post-permutation positions q*32 .. q*32+31 of the
-// block in registers.  The permutation gather reads LDS through a per-lane table that also
-// carries the Rademacher sign, so gather, sign and bf16->fp32 widening cost one LDS read and
-// one VALU op per element.  The Walsh-Hadamard butterflies over the five register bits of the
-// position run in registers; the two remaining stages cross lanes of the quad with DPP
-// quad permutations.  Those two stages compute own + sign*partner, which leaves the upper
-// lane of each pair holding the negated butterfly output; that sign is fixed per lane
-// (sigma = (-1)^popcount(q)) and is folded into the per-row scale used by the encoder.
-// The row's squared norm is reduced deterministically (quad DPP, then a per-row pass over
-// the block partials in LDS), after which each lane encodes its 32 coordinates against the
-// fp32 thresholds and writes them packed: 32 codes are 4*b bytes, one vector store per lane.
+// Work mapping (h = 128).  A persistent workgroup owns R rows per iteration and loops over row
+// groups.  Rows are staged in LDS as raw bf16 with 16-byte coalesced loads.  The next group is
+// loaded into registers right after the current group's gathers and written over the staging
+// buffer at the end of the iteration, so the HBM reads overlap the butterflies, the norm
+// reduction and the encoder, and the gather offsets stay loop-invariant registers.  Every
+// 128-block of a row belongs to one quad of lanes; lane q of the quad holds the 32 consecutive
+// post-permutation positions q*32 .. q*32+31.
+//
+// Per element the hot loop costs:
+//   gather       one LDS u16 read through a per-lane table of byte offsets (the permutation);
+//   sign         the Rademacher signs are XORed into the bf16 sign bits of the staged words (the
+//                plan carries a per-source-position mask, sign of the position the element moves
+//                to), half an op per element;
+//   widening and the first butterfly stage together: one v_dot2_f32_bf16 of a gathered bf16
+//                pair (y0, y1) with (1, 1) or (1, -1) gives y0 + y1 or y0 - y1 exactly in fp32;
+//   row norm     half a v_dot2 (the pair against itself; the rotation is orthogonal, so the sum of
+//                squares of the gathered inputs is the squared norm of the rotated row);
+//   butterflies  four more in-register stages and two stages across the quad, each one fused
+//                v_fmac_f32_dpp computing own + sign*partner.  That leaves the upper lane of each
+//                pair holding the negated output; the sign is fixed per lane,
+//                sigma = (-1)^popcount(q), and is folded into the per-row encoder scale;
+//   encode       t = fma(z, a, c) maps the coordinate to cells of a lookup table in LDS whose cells
+//                are narrower than the smallest threshold gap; one 8-byte read gives the cell's base
+//                code and its threshold (if any), so code = base + (t >= threshold);
+//   pack         one shift-or; 32 codes leave as one 4*b-byte vector store per lane.
+// The row's squared norm is reduced deterministically: quad DPP sums, per-block partials in LDS,
+// then one wave per row.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -25,12 +39,44 @@ namespace orbit {
 
 namespace {
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kEncOff = 32768;  // byte offset of the encoder table (the row buffer comes first)
+
 template <int CTRL>
 __device__ __forceinline__ float quad_perm(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 constexpr int kQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
 constexpr int kQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
+
+// z[r] <- z[r] + sgn * z[r] of the partner lane, for 16 registers, as fused DPP FMACs.  The compiler
+// cannot fuse mov_dpp into the tied-operand fmac, so this is written out; the leading s_nop covers
+// the two wait states a DPP read needs after a VALU write of its source.
+#define ORBIT_DPP_FMAC16(Z, B, SGN, PERM)                                                          \
+    asm volatile("s_nop 1\n"                                                                      \
+                 "v_fmac_f32_dpp %0, %0, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %1, %1, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %2, %2, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %3, %3, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %4, %4, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %5, %5, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %6, %6, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %7, %7, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %8, %8, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %9, %9, %16 " PERM " row_mask:0xf bank_mask:0xf\n"               \
+                 "v_fmac_f32_dpp %10, %10, %16 " PERM " row_mask:0xf bank_mask:0xf\n"             \
+                 "v_fmac_f32_dpp %11, %11, %16 " PERM " row_mask:0xf bank_mask:0xf\n"             \
+                 "v_fmac_f32_dpp %12, %12, %16 " PERM " row_mask:0xf bank_mask:0xf\n"             \
+                 "v_fmac_f32_dpp %13, %13, %16 " PERM " row_mask:0xf bank_mask:0xf\n"             \
+                 "v_fmac_f32_dpp %14, %14, %16 " PERM " row_mask:0xf bank_mask:0xf\n"             \
+                 "v_fmac_f32_dpp %15, %15, %16 " PERM " row_mask:0xf bank_mask:0xf\n"             \
+                 : "+v"(Z[B + 0]), "+v"(Z[B + 1]), "+v"(Z[B + 2]), "+v"(Z[B + 3]), "+v"(Z[B + 4]),    \
+                   "+v"(Z[B + 5]), "+v"(Z[B + 6]), "+v"(Z[B + 7]), "+v"(Z[B + 8]), "+v"(Z[B + 9]),    \
+                   "+v"(Z[B + 10]), "+v"(Z[B + 11]), "+v"(Z[B + 12]), "+v"(Z[B + 13]),              \
+                   "+v"(Z[B + 14]), "+v"(Z[B + 15])                                                  \
+                 : "v"(SGN))
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -44,37 +90,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
     return (uint16_t)(b >> 16);
 }
 
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
+
 template <int BITS>
-__device__ __forceinline__ void store_codes(uint8_t* dst, const int (&code)[32]) {
+__device__ __forceinline__ void store_packed(uint8_t* dst, const uint32_t (&w)[4]) {
     if constexpr (BITS == 4) {
-        uint32_t w[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            uint32_t v = 0;
-#pragma unroll
-            for (int t = 0; t < 8; ++t) v |= (uint32_t)code[8 * i + t] << (4 * t);
-            w[i] = v;
-        }
         *(uint4*)dst = make_uint4(w[0], w[1], w[2], w[3]);
     } else if constexpr (BITS == 2) {
-        uint32_t w[2];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            uint32_t v = 0;
-#pragma unroll
-            for (int t = 0; t < 16; ++t) v |= (uint32_t)code[16 * i + t] << (2 * t);
-            w[i] = v;
-        }
         *(uint2*)dst = make_uint2(w[0], w[1]);
     } else {
-        static_assert(BITS == 3, "bits");
-        uint32_t w[3] = {0u, 0u, 0u};
-#pragma unroll
-        for (int r = 0; r < 32; ++r) {
-            const int pos = 3 * r, wi = pos >> 5, sh = pos & 31;
-            w[wi] |= (uint32_t)code[r] << sh;
-            if (sh > 29) w[wi + 1] |= (uint32_t)code[r] >> (32 - sh);
-        }
         uint32_t* d = (uint32_t*)dst;
         d[0] = w[0];
         d[1] = w[1];
@@ -82,59 +108,85 @@ __device__ __forceinline__ void store_codes(uint8_t* dst, const int (&code)[32])
     }
 }
 
-template <int BITS, bool NORM_BF16>
-__global__ __launch_bounds__(512) void rpbh_quantize_kernel(QuantParams p) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    constexpr int NTHR = (1 << BITS) - 1;
-    const int K = p.K, nb = p.nb, R = p.R;
-    uint16_t* rows = (uint16_t*)smem;                       // R x K bf16
-    float* part = (float*)(smem + (size_t)R * K * 2);       // R x nb block partial sums
-    float* rowss = part + R * nb;                           // R row sums
-    const int tid = threadIdx.x, T = blockDim.x;
-    const int task = tid >> 2, q = tid & 3;
-    const int rg = task / nb, blk = task - rg * nb;
-    const bool active = task < R * nb;
+// LSB-first packing of code r (0..31) into the 4*BITS-byte group.
+template <int BITS>
+__device__ __forceinline__ void pack_code(uint32_t (&w)[4], int r, uint32_t code) {
+    const int pos = BITS * r, wi = pos >> 5, sh = pos & 31;
+    w[wi] |= code << sh;
+    if (sh + BITS > 32) w[wi + 1] |= code >> (32 - sh);
+}
 
-    uint32_t meta[32];
-    if (active) {
-        const uint4* src = (const uint4*)(p.meta + blk * 128 + q * 32);
+template <int BITS, bool NORM_BF16>
+struct Quantizer {
+    const QuantParams& p;
+    unsigned char* smem;
+    int tid, T, q, rg, blk;
+    bool active;
+    uint32_t addr[32];   // byte offset of each gathered element inside the staged group
+    float sigma;
+    int cpr;             // 16-byte chunks per row
+
+    __device__ __forceinline__ int rows_of(int g) const { return (int)min((int64_t)p.R, p.M - (int64_t)g * p.R); }
+
+    // Staging: the R rows of a group sit back to back in LDS, so 16-byte chunk c of the group lands
+    // at LDS byte 16*c and takes sign-mask words 4c..4c+3 (the mask is replicated per row slot).
+    // goff[k] is the global byte offset of this lane's chunk k from the group's first row.
+    uint32_t goff[4];
+
+    // The per-chunk offsets go through an empty asm so that the compiler recomputes the few
+    // address operations per iteration instead of hoisting 64-bit pointers out of the loop (which
+    // costs more registers than the loop body can spare).
+    __device__ __forceinline__ void load_group(int g, u32x4 (&pf)[4]) const {
+        const int lim = rows_of(g) * cpr;
+        const char* base = (const char*)p.X + (int64_t)g * p.R * p.ldx * 2;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            uint4 v = src[i];
-            meta[4 * i] = v.x;
-            meta[4 * i + 1] = v.y;
-            meta[4 * i + 2] = v.z;
-            meta[4 * i + 3] = v.w;
+        for (int k = 0; k < 4; ++k) {
+            uint32_t off = goff[k];
+            asm volatile("" : "+v"(off));
+            if (tid + k * T < lim) pf[k] = __builtin_nontemporal_load((const u32x4*)(base + off));
         }
     }
-    const float sgn1 = (q & 1) ? -1.f : 1.f;
-    const float sgn2 = (q & 2) ? -1.f : 1.f;
-    const float sigma = sgn1 * sgn2;
-    const int chunks = K >> 3;  // 16-byte chunks per row
-    const int64_t code_row_bytes = (int64_t)K * BITS / 8;
 
-    for (int g = blockIdx.x; g < p.ngroups; g += gridDim.x) {
-        const int64_t row0 = (int64_t)g * R;
-        const int nrows = (int)min((int64_t)R, p.M - row0);
-        for (int c = tid; c < nrows * chunks; c += T) {
-            const int r = c / chunks, o = c - r * chunks;
-            const uint4 v = *(const uint4*)(p.X + (row0 + r) * p.ldx + (int64_t)o * 8);
-            *(uint4*)(rows + (size_t)r * K + (size_t)o * 8) = v;
+    // applies the Rademacher sign masks of the staged positions and writes the group to LDS
+    __device__ __forceinline__ void store_group(int g, const u32x4 (&pf)[4]) const {
+        const int lim = rows_of(g) * cpr;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            int c = tid + k * T;
+            asm volatile("" : "+v"(c));
+            if (c < lim) *(u32x4*)(smem + 16 * c) = pf[k] ^ *(const u32x4*)(p.smask + 4 * c);
         }
-        __syncthreads();
+    }
 
+    __device__ __forceinline__ void iteration(int g) {
+        const int next = g + gridDim.x;
+        u32x4 pf[4];
+
+        const int K = p.K, nb = p.nb;
+        const int nrows = rows_of(g);
+        const int64_t row0 = (int64_t)g * p.R;
         const bool live = active && rg < nrows;
+        float* part = (float*)(smem + kEncOff + p.ncell * 8);
+        float* rowss = part + p.R * nb;
         float z[32];
         if (live) {
-            const unsigned char* myrow = (const unsigned char*)(rows + (size_t)rg * K);
+            uint32_t P[16];
 #pragma unroll
-            for (int r = 0; r < 32; ++r) {
-                const uint32_t m = meta[r];
-                const uint32_t b = *(const uint16_t*)(myrow + (m & 0xFFFFu));
-                z[r] = __uint_as_float((b << 16) ^ (m & 0x80000000u));
+            for (int i = 0; i < 16; ++i) {
+                const uint32_t lo = *(const uint16_t*)(smem + addr[2 * i]);
+                const uint32_t hi = *(const uint16_t*)(smem + addr[2 * i + 1]);
+                P[i] = lo | (hi << 16);
+            }
+            if (next < p.ngroups) load_group(next, pf);
+            float ss = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                z[2 * i] = dot2(P[i], 0x3F803F80u, 0.f);      // (+1, +1)
+                z[2 * i + 1] = dot2(P[i], 0xBF803F80u, 0.f);  // (+1, -1) on (lo, hi)
+                ss = dot2(P[i], P[i], ss);
             }
 #pragma unroll
-            for (int s = 1; s < 32; s <<= 1) {
+            for (int s = 2; s < 32; s <<= 1) {
 #pragma unroll
                 for (int r = 0; r < 32; ++r) {
                     if (r & s) continue;
@@ -143,16 +195,17 @@ __global__ __launch_bounds__(512) void rpbh_quantize_kernel(QuantParams p) {
                     z[r + s] = a - b;
                 }
             }
-#pragma unroll
-            for (int r = 0; r < 32; ++r) z[r] = fmaf(quad_perm<kQuadXor1>(z[r]), sgn1, z[r]);
-#pragma unroll
-            for (int r = 0; r < 32; ++r) z[r] = fmaf(quad_perm<kQuadXor2>(z[r]), sgn2, z[r]);
-            float ss = 0.f;
-#pragma unroll
-            for (int r = 0; r < 32; ++r) ss = fmaf(z[r], z[r], ss);
+            const float sgn1 = (q & 1) ? -1.f : 1.f;
+            const float sgn2 = (q & 2) ? -1.f : 1.f;
+            ORBIT_DPP_FMAC16(z, 0, sgn1, "quad_perm:[1,0,3,2]");
+            ORBIT_DPP_FMAC16(z, 16, sgn1, "quad_perm:[1,0,3,2]");
+            ORBIT_DPP_FMAC16(z, 0, sgn2, "quad_perm:[2,3,0,1]");
+            ORBIT_DPP_FMAC16(z, 16, sgn2, "quad_perm:[2,3,0,1]");
             ss += quad_perm<kQuadXor1>(ss);
             ss += quad_perm<kQuadXor2>(ss);
             if (q == 0) part[rg * nb + blk] = ss;
+        } else if (next < p.ngroups) {
+            load_group(next, pf);
         }
         __syncthreads();
 
@@ -162,8 +215,8 @@ __global__ __launch_bounds__(512) void rpbh_quantize_kernel(QuantParams p) {
             for (int i = lane; i < nb; i += 64) acc += part[r * nb + i];
             acc = wave_sum(acc);
             if (lane == 0) {
-                rowss[r] = acc;
-                const float s = sqrtf(acc * (1.0f / 128.0f));
+                const float s = sqrtf(acc);
+                rowss[r] = s;
                 if constexpr (NORM_BF16)
                     ((uint16_t*)p.norm)[row0 + r] = f32_to_bf16_rne(s);
                 else
@@ -173,30 +226,95 @@ __global__ __launch_bounds__(512) void rpbh_quantize_kernel(QuantParams p) {
         __syncthreads();
 
         if (live) {
-            const float s = sqrtf(rowss[rg] * (1.0f / 128.0f));
-            // u = z / (s + eps) with z = z_unnormalised / sqrt(128); sigma undoes the lane sign
-            const float scale = sigma / ((s + p.eps) * 11.313708498984761f);
-            int code[32];
+            const float s = rowss[rg];
+            // u = z / (s + eps) with z = z_unnormalised / sqrt(128); t = u / w + center
+            const float a = sigma * p.enc_inv_w / ((s + p.eps) * 11.313708498984761f);
+            const float c = p.enc_center;
+            const unsigned char* tab = smem + kEncOff;
+            uint32_t w[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-            for (int r = 0; r < 32; ++r) {
-                const float u = z[r] * scale;
-                int c = 0;
+            for (int r0 = 0; r0 < 32; r0 += 8) {
+                float t[8];
+                uint2 e[8];
 #pragma unroll
-                for (int j = 0; j < NTHR; ++j) c += (u >= p.thr[j]) ? 1 : 0;
-                code[r] = c;
+                for (int i = 0; i < 8; ++i) {
+                    t[i] = fmaf(z[r0 + i], a, c);
+                    e[i] = *(const uint2*)(tab + (uint32_t)t[i] * 8);
+                }
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    pack_code<BITS>(w, r0 + i, e[i].y + (t[i] >= __uint_as_float(e[i].x) ? 1u : 0u));
             }
-            uint8_t* dst = p.codes + (row0 + rg) * code_row_bytes + (int64_t)(blk * 4 + q) * 4 * BITS;
-            store_codes<BITS>(dst, code);
+            uint8_t* dst = p.codes + (row0 + rg) * ((int64_t)K * BITS / 8) + (int64_t)(blk * 4 + q) * 4 * BITS;
+            store_packed<BITS>(dst, w);
         }
-        __syncthreads();
+        __syncthreads();  // every lane is past its gathers: the staging buffer takes the next group
+        if (next < p.ngroups) {
+            store_group(next, pf);
+            __syncthreads();
+        }
+    }
+};
+
+template <int BITS, bool NORM_BF16>
+__global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    Quantizer<BITS, NORM_BF16> Q{p, smem};
+    Q.tid = threadIdx.x;
+    Q.T = blockDim.x;
+    const int task = Q.tid >> 2;
+    Q.q = Q.tid & 3;
+    Q.rg = task / p.nb;
+    Q.blk = task - Q.rg * p.nb;
+    Q.active = task < p.R * p.nb;
+    Q.cpr = p.K >> 3;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int c = Q.tid + k * Q.T, r = c / Q.cpr;
+        Q.goff[k] = (uint32_t)(r * p.ldx * 2 + (c - r * Q.cpr) * 16);
+    }
+    Q.sigma = ((Q.q & 1) ? -1.f : 1.f) * ((Q.q & 2) ? -1.f : 1.f);
+
+    // encoder table -> LDS
+    uint32_t* tab = (uint32_t*)(smem + kEncOff);
+    for (int i = Q.tid; i < 2 * p.ncell; i += Q.T) tab[i] = p.enc[i];
+
+    if (Q.active) {
+        const uint4* src = (const uint4*)(p.meta + Q.blk * 128 + Q.q * 32);
+        const uint32_t rowoff = (uint32_t)(Q.rg * p.K * 2);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint4 v = src[i];
+            const uint32_t m[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) Q.addr[4 * i + k] = rowoff + (m[k] & 0xFFFFu);
+        }
+    }
+
+    if (blockIdx.x < p.ngroups) {
+        u32x4 pf[4];
+        Q.load_group(blockIdx.x, pf);
+        Q.store_group(blockIdx.x, pf);
+    }
+    __syncthreads();
+    for (int g = blockIdx.x; g < p.ngroups; g += gridDim.x) Q.iteration(g);
+}
+
+template <int BITS, bool NB>
+void set_smem_limit() {
+    static bool done = false;
+    if (!done) {
+        (void)hipFuncSetAttribute((const void*)rpbh_quantize_kernel<BITS, NB>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            160 * 1024);
+        done = true;
     }
 }
 
 }  // namespace
 
-size_t quant_smem_bytes(int K, int R) {
+size_t quant_smem_bytes(int K, int R, int ncell) {
     const int nb = K / 128;
-    return (size_t)R * K * 2 + (size_t)R * nb * 4 + (size_t)R * 4;
+    return (size_t)kEncOff + (size_t)ncell * 8 + (size_t)R * nb * 4 + (size_t)R * 4;
 }
 
 int quant_rows_per_group(int K) {
@@ -206,9 +324,12 @@ int quant_rows_per_group(int K) {
 
 hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, int grid, hipStream_t stream) {
     const int threads = ((p.R * p.nb * 4 + 63) / 64) * 64;
-    const size_t smem = quant_smem_bytes(p.K, p.R);
-#define ORBIT_LAUNCH(B, NB)                                                                   \
-    hipLaunchKernelGGL((rpbh_quantize_kernel<B, NB>), dim3(grid), dim3(threads), smem, stream, p)
+    const size_t smem = quant_smem_bytes(p.K, p.R, p.ncell);
+#define ORBIT_LAUNCH(B, NB)                                                                        \
+    do {                                                                                           \
+        set_smem_limit<B, NB>();                                                                   \
+        hipLaunchKernelGGL((rpbh_quantize_kernel<B, NB>), dim3(grid), dim3(threads), smem, stream, p); \
+    } while (0)
     if (norm_bf16) {
         if (bits == 2) ORBIT_LAUNCH(2, true);
         else if (bits == 3) ORBIT_LAUNCH(3, true);

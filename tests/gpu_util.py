@@ -87,3 +87,30 @@ def qlinear_oracle_fp16(xc, xs, cba_bits, wc, wr, cbw_bits, K):
 
 def rel_frobenius(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def near_tie_flip_bound(cx, s, Ux, la, tha, cw, r, Uw, lw, thw, band=TIE_BAND):
+    """Frobenius bound on how far the quantized layer can move when every coordinate within
+    `band` of a threshold takes the neighbouring code instead (the oracle's own codes, levels
+    and norms only).  Flipping weight code (i, k) by one level changes column i by
+    r_i * dL * (s_n La[cx[n, k]])_n; flipping activation code (n, k) changes row n by
+    s_n * dL * (r_i Lw[cw[i, k]])_i.  The triangle inequality over flips gives the bound."""
+    la, lw = np.asarray(la), np.asarray(lw)
+
+    def step(U, th, codes, levels):
+        # level difference to the neighbour across the nearest threshold, 0 off near-ties
+        near = oracle.near_tie_mask(U, th, band)
+        idx = np.searchsorted(th, U)                        # threshold index at or above u
+        lo = np.clip(idx - 1, 0, len(th) - 1)
+        hi = np.clip(idx, 0, len(th) - 1)
+        j = np.where(np.abs(U - th[lo]) <= np.abs(U - th[hi]), lo, hi)   # nearest threshold
+        d = np.abs(levels[j + 1] - levels[j])
+        return np.where(near, d, 0.0)
+
+    dw = step(Uw, thw, cw, lw)                              # [N, K]
+    da = step(Ux, tha, cx, la)                              # [M, K]
+    A = s[:, None] * la[cx]                                 # [M, K]
+    B = r[:, None] * lw[cw]                                 # [N, K]
+    col = r * (dw @ np.linalg.norm(A, axis=0))              # per output column i
+    row = s * (da @ np.linalg.norm(B, axis=0))              # per output row n
+    return float(np.sqrt(np.sum(col ** 2)) + np.sqrt(np.sum(row ** 2)))
