@@ -18,10 +18,11 @@ struct QuantParams {
     int K, nb, R;          // input dim, K/128 blocks, rows staged per workgroup iteration
     int ngroups;           // ceil(M / R)
     float eps;
-    const uint32_t* enc;   // encoder table: ncell pairs (threshold in cell units as fp32 bits, base code)
+    const float* enc;      // encoder table: per-cell bias (see the codebook's encoder table)
     int ncell;
     float enc_inv_w;       // cells per unit of the normalized coordinate
     float enc_center;      // cell coordinate of u = 0
+    uint32_t one_one;      // bf16 pair (1.0, 1.0), 0x3F803F80
 };
 
 int quant_rows_per_group(int K);

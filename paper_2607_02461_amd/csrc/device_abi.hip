@@ -75,19 +75,19 @@ orbit_status plan_meta(orbit_plan p, int dev, const uint32_t** out) {
 }
 
 // The codebook's encoder table on device `dev`, uploaded on first use.
-orbit_status codebook_enc(orbit_codebook c, int dev, const uint32_t** out) {
+orbit_status codebook_enc(orbit_codebook c, int dev, const float** out) {
     std::lock_guard<std::mutex> lk(c->mu);
     if (!c->dev_enc[dev]) {
-        const size_t bytes = c->enc.entries.size() * sizeof(uint32_t);
+        const size_t bytes = c->enc.bias.size() * sizeof(float);
         void* d = nullptr;
         hipError_t e = hipMalloc(&d, bytes);
         if (e != hipSuccess) return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "codebook upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
-        e = hipMemcpy(d, c->enc.entries.data(), bytes, hipMemcpyHostToDevice);
+        e = hipMemcpy(d, c->enc.bias.data(), bytes, hipMemcpyHostToDevice);
         if (e != hipSuccess) {
             (void)hipFree(d);
             return hip_fail(e, "codebook upload: hipMemcpy");
         }
-        c->dev_enc[dev] = (uint32_t*)d;
+        c->dev_enc[dev] = (float*)d;
     }
     *out = c->dev_enc[dev];
     return ORBIT_OK;
@@ -119,7 +119,7 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     const uint32_t* meta = nullptr;
     st = plan_meta(p, dev, &meta);
     if (st != ORBIT_OK) return st;
-    const uint32_t* enc = nullptr;
+    const float* enc = nullptr;
     st = codebook_enc(cb, dev, &enc);
     if (st != ORBIT_OK) return st;
     if (cb->enc.ncell > kQuantMaxCells)
@@ -142,6 +142,7 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     q.ncell = cb->enc.ncell;
     q.enc_inv_w = cb->enc.inv_w;
     q.enc_center = cb->enc.center;
+    q.one_one = 0x3F803F80u;
     // two workgroups fit a compute unit (LDS: double row buffer + encoder table)
     const int grid = (int)std::min<int64_t>(q.ngroups, (int64_t)info.cus * 2);
     hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, grid, (hipStream_t)stream);

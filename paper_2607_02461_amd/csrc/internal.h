@@ -32,14 +32,17 @@ struct orbit_plan_s {
 
 // Encoder lookup table over the normalized coordinate u in [-kEncRange, kEncRange]: cell c covers
 // u in [c*w - kEncRange, (c+1)*w - kEncRange) with w below the smallest threshold spacing, so a cell
-// holds at most one threshold.  In cell coordinates t = (u + kEncRange) / w, the code of t in cell c
-// is base[c] + (t >= tthr[c]), with tthr = +inf for cells without a threshold.
+// holds at most one threshold.  In cell coordinates t = (u + kEncRange) / w the code is
+// round-to-nearest-even(0.5*t + bias[cell]) with
+//     bias = base + 0.5 - 0.5*T          in a cell whose threshold sits at T (code base or base+1),
+//     bias = base - 0.25 - 0.5*c         in a cell without one (0.5*t + bias stays within 0.25 of base),
+// where base is the number of thresholds below the cell.
 constexpr double kEncRange = 1.001;  // |u| <= 1 up to rounding
 struct EncTable {
     float inv_w = 0.f;   // 1 / w
     float center = 0.f;  // kEncRange / w
     int32_t ncell = 0;
-    std::vector<uint32_t> entries;  // ncell pairs: (bits of tthr as fp32, base code)
+    std::vector<float> bias;
 };
 
 // C^(d,b): ascending levels, midpoint thresholds, fp16 image of the levels.
@@ -51,7 +54,7 @@ struct orbit_codebook_s {
     std::vector<uint16_t> lut_f16;
     EncTable enc;
     std::mutex mu;
-    uint32_t* dev_enc[orbit::kMaxDevices] = {};
+    float* dev_enc[orbit::kMaxDevices] = {};
 };
 
 namespace orbit {

@@ -94,6 +94,14 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
 }
 
+// First butterfly stage from a bf16 pair (y0, y1): y0 + y1 and y0 - y1 as the three-operand
+// v_dot2_f32_bf16 against (1, 1) held in an SGPR, with neg_hi giving (1, -1).  (The accumulating
+// two-operand form the compiler picks would need its destination zeroed first.)
+__device__ __forceinline__ void stage1(uint32_t P, uint32_t one_one, float& sum, float& diff) {
+    asm("v_dot2_f32_bf16 %0, %1, %2, 0" : "=v"(sum) : "v"(P), "s"(one_one));
+    asm("v_dot2_f32_bf16 %0, %1, %2, 0 neg_hi:[0,1,0]" : "=v"(diff) : "v"(P), "s"(one_one));
+}
+
 template <int BITS>
 __device__ __forceinline__ void store_packed(uint8_t* dst, const uint32_t (&w)[4]) {
     if constexpr (BITS == 4) {
@@ -108,12 +116,70 @@ __device__ __forceinline__ void store_packed(uint8_t* dst, const uint32_t (&w)[4
     }
 }
 
-// LSB-first packing of code r (0..31) into the 4*BITS-byte group.
+// y -> round-to-nearest-even(y) saturated to [0, 255], inserted as byte K of `into`
+template <int K>
+__device__ __forceinline__ uint32_t code_byte(float y, uint32_t into) {
+    return __builtin_amdgcn_cvt_pk_u8_f32(y, K, into);
+}
+
+// Packs 32 codes, given as values y whose nearest integer is the code, LSB-first into 4*BITS
+// bytes.  v_cvt_pk_u8_f32 converts a value and inserts it as one byte of a word in a single op;
+// the codes are spread over bytes so that a few shifts and ORs close the gaps between them.
 template <int BITS>
-__device__ __forceinline__ void pack_code(uint32_t (&w)[4], int r, uint32_t code) {
-    const int pos = BITS * r, wi = pos >> 5, sh = pos & 31;
-    w[wi] |= code << sh;
-    if (sh + BITS > 32) w[wi + 1] |= code >> (32 - sh);
+__device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[4]) {
+    if constexpr (BITS == 4) {
+        // bytes of A = codes 8i, 8i+2, 8i+4, 8i+6 and of B = codes 8i+1, 8i+3, ...: A | B << 4
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float* v = y + 8 * i;
+            uint32_t A = code_byte<0>(v[0], 0u), B = code_byte<0>(v[1], 0u);
+            A = code_byte<1>(v[2], A);
+            B = code_byte<1>(v[3], B);
+            A = code_byte<2>(v[4], A);
+            B = code_byte<2>(v[5], B);
+            A = code_byte<3>(v[6], A);
+            B = code_byte<3>(v[7], B);
+            w[i] = A | (B << 4);
+        }
+        return;
+    } else if constexpr (BITS == 2) {
+        // byte j of D_k holds code 16i + 4j + k: D_0 | D_1 << 2 | D_2 << 4 | D_3 << 6
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const float* v = y + 16 * i;
+            uint32_t D[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                uint32_t d = code_byte<0>(v[k], 0u);
+                d = code_byte<1>(v[4 + k], d);
+                d = code_byte<2>(v[8 + k], d);
+                D[k] = code_byte<3>(v[12 + k], d);
+            }
+            w[i] = D[0] | (D[1] << 2) | (D[2] << 4) | (D[3] << 6);
+        }
+        w[2] = w[3] = 0u;
+    } else {
+        static_assert(BITS == 3, "bits");
+        // 8 codes = 24 bits: codes 2j, 2j+1 share byte j of P (6 bits), then the gaps close
+        uint32_t g[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float* v = y + 8 * i;
+            uint32_t A = code_byte<0>(v[0], 0u), B = code_byte<0>(v[1], 0u);
+            A = code_byte<1>(v[2], A);
+            B = code_byte<1>(v[3], B);
+            A = code_byte<2>(v[4], A);
+            B = code_byte<2>(v[5], B);
+            A = code_byte<3>(v[6], A);
+            B = code_byte<3>(v[7], B);
+            const uint32_t P = A | (B << 3);
+            g[i] = (P & 0x3Fu) | ((P >> 2) & 0xFC0u) | ((P >> 4) & 0x3F000u) | ((P >> 6) & 0xFC0000u);
+        }
+        w[0] = g[0] | (g[1] << 24);
+        w[1] = (g[1] >> 8) | (g[2] << 16);
+        w[2] = (g[2] >> 16) | (g[3] << 8);
+        w[3] = 0u;
+    }
 }
 
 template <int BITS, bool NORM_BF16>
@@ -121,7 +187,7 @@ struct Quantizer {
     const QuantParams& p;
     unsigned char* smem;
     int tid, T, q, rg, blk;
-    bool active;
+    bool active;         // lane owns a (row slot, block) of the group
     uint32_t addr[32];   // byte offset of each gathered element inside the staged group
     float sigma;
     int cpr;             // 16-byte chunks per row
@@ -158,55 +224,54 @@ struct Quantizer {
         }
     }
 
+    // One row group.  Every lane runs the arithmetic (lanes without a block of a valid row work on
+    // harmless LDS data); only the stores are guarded, so the hot path has no divergence.
     __device__ __forceinline__ void iteration(int g) {
         const int next = g + gridDim.x;
-        u32x4 pf[4];
-
-        const int K = p.K, nb = p.nb;
+        const int nb = p.nb;
         const int nrows = rows_of(g);
         const int64_t row0 = (int64_t)g * p.R;
-        const bool live = active && rg < nrows;
-        float* part = (float*)(smem + kEncOff + p.ncell * 8);
+        const bool owner = active && rg < nrows;
+        float* part = (float*)(smem + kEncOff + p.ncell * 4);
         float* rowss = part + p.R * nb;
-        float z[32];
-        if (live) {
-            uint32_t P[16];
+
+        // gathered pairs: element 2i in the low half, 2i+1 in the high half of P[i]
+        uint32_t P[16];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const uint32_t lo = *(const uint16_t*)(smem + addr[2 * i]);
-                const uint32_t hi = *(const uint16_t*)(smem + addr[2 * i + 1]);
-                P[i] = lo | (hi << 16);
-            }
-            if (next < p.ngroups) load_group(next, pf);
-            float ss = 0.f;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                z[2 * i] = dot2(P[i], 0x3F803F80u, 0.f);      // (+1, +1)
-                z[2 * i + 1] = dot2(P[i], 0xBF803F80u, 0.f);  // (+1, -1) on (lo, hi)
-                ss = dot2(P[i], P[i], ss);
-            }
-#pragma unroll
-            for (int s = 2; s < 32; s <<= 1) {
-#pragma unroll
-                for (int r = 0; r < 32; ++r) {
-                    if (r & s) continue;
-                    const float a = z[r], b = z[r + s];
-                    z[r] = a + b;
-                    z[r + s] = a - b;
-                }
-            }
-            const float sgn1 = (q & 1) ? -1.f : 1.f;
-            const float sgn2 = (q & 2) ? -1.f : 1.f;
-            ORBIT_DPP_FMAC16(z, 0, sgn1, "quad_perm:[1,0,3,2]");
-            ORBIT_DPP_FMAC16(z, 16, sgn1, "quad_perm:[1,0,3,2]");
-            ORBIT_DPP_FMAC16(z, 0, sgn2, "quad_perm:[2,3,0,1]");
-            ORBIT_DPP_FMAC16(z, 16, sgn2, "quad_perm:[2,3,0,1]");
-            ss += quad_perm<kQuadXor1>(ss);
-            ss += quad_perm<kQuadXor2>(ss);
-            if (q == 0) part[rg * nb + blk] = ss;
-        } else if (next < p.ngroups) {
-            load_group(next, pf);
+        for (int i = 0; i < 16; ++i) {
+            const uint32_t lo = *(const uint16_t*)(smem + addr[2 * i]);
+            const uint32_t hi = *(const uint16_t*)(smem + addr[2 * i + 1]);
+            P[i] = lo | (hi << 16);
         }
+        u32x4 pf[4];
+        if (next < p.ngroups) load_group(next, pf);
+
+        float z[32];
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            stage1(P[i], p.one_one, z[2 * i], z[2 * i + 1]);
+            ss = dot2(P[i], P[i], ss);
+        }
+#pragma unroll
+        for (int s = 2; s < 32; s <<= 1) {
+#pragma unroll
+            for (int r = 0; r < 32; ++r) {
+                if (r & s) continue;
+                const float a = z[r], b = z[r + s];
+                z[r] = a + b;
+                z[r + s] = a - b;
+            }
+        }
+        const float sgn1 = (q & 1) ? -1.f : 1.f;
+        const float sgn2 = (q & 2) ? -1.f : 1.f;
+        ORBIT_DPP_FMAC16(z, 0, sgn1, "quad_perm:[1,0,3,2]");
+        ORBIT_DPP_FMAC16(z, 16, sgn1, "quad_perm:[1,0,3,2]");
+        ORBIT_DPP_FMAC16(z, 0, sgn2, "quad_perm:[2,3,0,1]");
+        ORBIT_DPP_FMAC16(z, 16, sgn2, "quad_perm:[2,3,0,1]");
+        ss += quad_perm<kQuadXor1>(ss);
+        ss += quad_perm<kQuadXor2>(ss);
+        if (owner && q == 0) part[rg * nb + blk] = ss;
         __syncthreads();
 
         const int wave = tid >> 6, lane = tid & 63, nwaves = T >> 6;
@@ -225,30 +290,22 @@ struct Quantizer {
         }
         __syncthreads();
 
-        if (live) {
-            const float s = rowss[rg];
-            // u = z / (s + eps) with z = z_unnormalised / sqrt(128); t = u / w + center
-            const float a = sigma * p.enc_inv_w / ((s + p.eps) * 11.313708498984761f);
-            const float c = p.enc_center;
-            const unsigned char* tab = smem + kEncOff;
-            uint32_t w[4] = {0u, 0u, 0u, 0u};
+        // u = z / (s + eps) with z = z_unnormalised / sqrt(128); t = u / w + center is the cell
+        // coordinate and round(0.5 t + bias[cell]) the code
+        const float s = rowss[owner ? rg : 0];
+        const float a = sigma * p.enc_inv_w / ((s + p.eps) * 11.313708498984761f);
+        const float c = p.enc_center;
+        const float* tab = (const float*)(smem + kEncOff);
+        float y[32];
 #pragma unroll
-            for (int r0 = 0; r0 < 32; r0 += 8) {
-                float t[8];
-                uint2 e[8];
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    t[i] = fmaf(z[r0 + i], a, c);
-                    e[i] = *(const uint2*)(tab + (uint32_t)t[i] * 8);
-                }
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    pack_code<BITS>(w, r0 + i, e[i].y + (t[i] >= __uint_as_float(e[i].x) ? 1u : 0u));
-            }
-            uint8_t* dst = p.codes + (row0 + rg) * ((int64_t)K * BITS / 8) + (int64_t)(blk * 4 + q) * 4 * BITS;
-            store_packed<BITS>(dst, w);
+        for (int r = 0; r < 32; ++r) {
+            const float t = fmaf(z[r], a, c);
+            y[r] = fmaf(t, 0.5f, tab[(uint32_t)t]);
         }
-        __syncthreads();  // every lane is past its gathers: the staging buffer takes the next group
+        uint32_t w[4];
+        pack_codes<BITS>(y, w);
+        if (owner)
+            store_packed<BITS>(p.codes + (row0 + rg) * ((int64_t)p.K * BITS / 8) + (int64_t)(blk * 4 + q) * 4 * BITS, w);
         if (next < p.ngroups) {
             store_group(next, pf);
             __syncthreads();
@@ -264,22 +321,22 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
     Q.T = blockDim.x;
     const int task = Q.tid >> 2;
     Q.q = Q.tid & 3;
-    Q.rg = task / p.nb;
-    Q.blk = task - Q.rg * p.nb;
     Q.active = task < p.R * p.nb;
+    Q.rg = Q.active ? task / p.nb : 0;
+    Q.blk = Q.active ? task - Q.rg * p.nb : 0;
     Q.cpr = p.K >> 3;
+    Q.sigma = ((Q.q & 1) ? -1.f : 1.f) * ((Q.q & 2) ? -1.f : 1.f);
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int c = Q.tid + k * Q.T, r = c / Q.cpr;
         Q.goff[k] = (uint32_t)(r * p.ldx * 2 + (c - r * Q.cpr) * 16);
     }
-    Q.sigma = ((Q.q & 1) ? -1.f : 1.f) * ((Q.q & 2) ? -1.f : 1.f);
 
     // encoder table -> LDS
-    uint32_t* tab = (uint32_t*)(smem + kEncOff);
-    for (int i = Q.tid; i < 2 * p.ncell; i += Q.T) tab[i] = p.enc[i];
+    float* tab = (float*)(smem + kEncOff);
+    for (int i = Q.tid; i < p.ncell; i += Q.T) tab[i] = p.enc[i];
 
-    if (Q.active) {
+    {
         const uint4* src = (const uint4*)(p.meta + Q.blk * 128 + Q.q * 32);
         const uint32_t rowoff = (uint32_t)(Q.rg * p.K * 2);
 #pragma unroll
@@ -287,7 +344,7 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
             const uint4 v = src[i];
             const uint32_t m[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-            for (int k = 0; k < 4; ++k) Q.addr[4 * i + k] = rowoff + (m[k] & 0xFFFFu);
+            for (int k = 0; k < 4; ++k) Q.addr[4 * i + k] = Q.active ? rowoff + m[k] : 0u;
         }
     }
 
@@ -314,7 +371,7 @@ void set_smem_limit() {
 
 size_t quant_smem_bytes(int K, int R, int ncell) {
     const int nb = K / 128;
-    return (size_t)kEncOff + (size_t)ncell * 8 + (size_t)R * nb * 4 + (size_t)R * 4;
+    return (size_t)kEncOff + (size_t)ncell * 4 + (size_t)R * nb * 4 + (size_t)R * 4;
 }
 
 int quant_rows_per_group(int K) {
