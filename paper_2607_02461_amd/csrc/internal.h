@@ -6,7 +6,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/orbitquant.h"
+#include "orbitquant.h"
 
 namespace orbit {
 

@@ -78,10 +78,17 @@ constexpr int kQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
                    "+v"(Z[B + 14]), "+v"(Z[B + 15])                                                  \
                  : "v"(SGN))
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+// Sum over the 64 lanes of a wave, the same value in every lane, in a fixed order: quad, half-row
+// and row sums by DPP, then the four row sums read out lane by lane.
+__device__ __forceinline__ float wave_total(float v) {
+    v += quad_perm<kQuadXor1>(v);
+    v += quad_perm<kQuadXor2>(v);
+    v += quad_perm<0x141>(v);  // row_half_mirror: lane l of 8 <- lane 7 - l
+    v += quad_perm<0x140>(v);  // row_mirror: lane l of 16 <- lane 15 - l
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
+           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
+           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
 }
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
@@ -233,7 +240,6 @@ struct Quantizer {
         const int64_t row0 = (int64_t)g * p.R;
         const bool owner = active && rg < nrows;
         float* part = (float*)(smem + kEncOff + p.ncell * 4);
-        float* rowss = part + p.R * nb;
 
         // gathered pairs: element 2i in the low half, 2i+1 in the high half of P[i]
         uint32_t P[16];
@@ -274,25 +280,28 @@ struct Quantizer {
         if (owner && q == 0) part[rg * nb + blk] = ss;
         __syncthreads();
 
-        const int wave = tid >> 6, lane = tid & 63, nwaves = T >> 6;
-        for (int r = wave; r < nrows; r += nwaves) {
+        // Row totals: each wave reduces the block partials of the rows its lanes hold (the same
+        // fixed-order sum in every wave), so no second barrier is needed.  The lane holding block 0
+        // of a row stores its norm.
+        const int lane = tid & 63;
+        const int r_first = __builtin_amdgcn_readfirstlane(rg);
+        const int r_last = __builtin_amdgcn_readlane(rg, 63);
+        float s = 0.f;
+        for (int r = r_first; r <= r_last && r < nrows; ++r) {
             float acc = 0.f;
             for (int i = lane; i < nb; i += 64) acc += part[r * nb + i];
-            acc = wave_sum(acc);
-            if (lane == 0) {
-                const float s = sqrtf(acc);
-                rowss[r] = s;
-                if constexpr (NORM_BF16)
-                    ((uint16_t*)p.norm)[row0 + r] = f32_to_bf16_rne(s);
-                else
-                    ((float*)p.norm)[row0 + r] = s;
-            }
+            const float tot = sqrtf(wave_total(acc));
+            if (rg == r) s = tot;
         }
-        __syncthreads();
+        if (owner && blk == 0 && q == 0) {
+            if constexpr (NORM_BF16)
+                ((uint16_t*)p.norm)[row0 + rg] = f32_to_bf16_rne(s);
+            else
+                ((float*)p.norm)[row0 + rg] = s;
+        }
 
         // u = z / (s + eps) with z = z_unnormalised / sqrt(128); t = u / w + center is the cell
         // coordinate and round(0.5 t + bias[cell]) the code
-        const float s = rowss[owner ? rg : 0];
         const float a = sigma * p.enc_inv_w / ((s + p.eps) * 11.313708498984761f);
         const float c = p.enc_center;
         const float* tab = (const float*)(smem + kEncOff);
@@ -322,8 +331,10 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
     const int task = Q.tid >> 2;
     Q.q = Q.tid & 3;
     Q.active = task < p.R * p.nb;
-    Q.rg = Q.active ? task / p.nb : 0;
-    Q.blk = Q.active ? task - Q.rg * p.nb : 0;
+    // lanes past the last block keep the row index their task would have (so a wave's rows are
+    // contiguous); every access they could make through it is guarded by `active`
+    Q.rg = task / p.nb;
+    Q.blk = task - Q.rg * p.nb;
     Q.cpr = p.K >> 3;
     Q.sigma = ((Q.q & 1) ? -1.f : 1.f) * ((Q.q & 2) ? -1.f : 1.f);
 #pragma unroll
