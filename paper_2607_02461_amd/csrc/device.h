@@ -42,6 +42,6 @@ struct GemmParams {
     uint16_t lut_w[16];    // fp16 levels (2^bw used)
 };
 
-hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, hipStream_t stream);
+hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, int cus, hipStream_t stream);
 
 }  // namespace orbit

@@ -226,7 +226,7 @@ orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const fl
         g.lut_a[j] = j < (1 << cb_a->bits) ? cb_a->lut_f16[j] : 0;
         g.lut_w[j] = j < (1 << cb_w->bits) ? cb_w->lut_f16[j] : 0;
     }
-    hipError_t e = launch_lut_gemm(g, cb_a->bits, cb_w->bits, (hipStream_t)stream);
+    hipError_t e = launch_lut_gemm(g, cb_a->bits, cb_w->bits, info.cus, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "orbit_qlinear");
     return ORBIT_OK;
 }

@@ -46,59 +46,68 @@ __device__ __forceinline__ ByteTables make_tables(const uint16_t* lut, int n) {
     return t;
 }
 
-// Four codes (one per byte of c4) -> four fp16 values as two fp16x2 words.
+// Canonical slot order.  The eight codes of each aligned group k0..k7 are written to eight
+// consecutive fp16 slots in the order k0 k2 k4 k6 k1 k3 k5 k7.  Both operands use the same order
+// for every bit width, so every MFMA still contracts matching k; the order is the one the 4-bit
+// decoder produces without any byte shuffling (even and odd nibbles of a code word).
+
+// Four 3-bit level indices (one per byte of sel) with a fourth bit per byte in hi8 (bit 2 of each
+// byte of s4, already placed) -> fp16 low and high bytes; for tables of at most eight levels the
+// combine step is skipped.
 template <int BITS>
-__device__ __forceinline__ void lookup4(uint32_t c4, const ByteTables& t, uint32_t& d0, uint32_t& d1) {
-    uint32_t lo, hi;
+__device__ __forceinline__ void lookup_bytes(uint32_t sel, uint32_t s4, const ByteTables& t, uint32_t& lo,
+                                             uint32_t& hi) {
     if constexpr (BITS <= 3) {
-        lo = __builtin_amdgcn_perm(t.lo[1], t.lo[0], c4);
-        hi = __builtin_amdgcn_perm(t.hi[1], t.hi[0], c4);
+        lo = __builtin_amdgcn_perm(t.lo[1], t.lo[0], sel);
+        hi = __builtin_amdgcn_perm(t.hi[1], t.hi[0], sel);
     } else {
-        const uint32_t sel = c4 & 0x07070707u;
-        const uint32_t mask = ((c4 >> 3) & 0x01010101u) * 0xFFu;
+        // levels 0..7 and 8..15 looked up separately, then byte i taken from the second table
+        // when that code's top bit is set (s4 byte i = i + 4 * bit)
         const uint32_t lo0 = __builtin_amdgcn_perm(t.lo[1], t.lo[0], sel);
         const uint32_t lo1 = __builtin_amdgcn_perm(t.lo[3], t.lo[2], sel);
         const uint32_t hi0 = __builtin_amdgcn_perm(t.hi[1], t.hi[0], sel);
         const uint32_t hi1 = __builtin_amdgcn_perm(t.hi[3], t.hi[2], sel);
-        lo = (mask & lo1) | (~mask & lo0);
-        hi = (mask & hi1) | (~mask & hi0);
+        lo = __builtin_amdgcn_perm(lo1, lo0, s4);
+        hi = __builtin_amdgcn_perm(hi1, hi0, s4);
     }
+}
+
+// low/high byte words of four values -> two fp16x2 words (values 0,1 and 2,3)
+__device__ __forceinline__ void interleave(uint32_t lo, uint32_t hi, uint32_t& d0, uint32_t& d1) {
     d0 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);  // [lo0 hi0 lo1 hi1]
     d1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);  // [lo2 hi2 lo3 hi3]
 }
 
-// 32 packed codes (4*BITS bytes, LSB-first) -> 32 fp16 values in out[16] (fp16x2 words).
+// Group g (codes 8g .. 8g+7) of 32 packed codes (4*BITS bytes, LSB-first) -> four fp16x2 words
+// in canonical slot order.
 template <int BITS>
-__device__ __forceinline__ void decode32(const uint32_t* w, const ByteTables& t, uint32_t (&out)[16]) {
+__device__ __forceinline__ void decode8(const uint32_t (&w)[4], int g, const ByteTables& t, uint32_t (&out)[4]) {
+    uint32_t ce, co;  // codes k0 k2 k4 k6 and k1 k3 k5 k7, one per byte (low BITS bits significant)
+    uint32_t se = 0, so = 0;
     if constexpr (BITS == 4) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const uint32_t even = w[i] & 0x0F0F0F0Fu;
-            const uint32_t odd = (w[i] >> 4) & 0x0F0F0F0Fu;
-            const uint32_t c0 = __builtin_amdgcn_perm(odd, even, 0x05010400u);  // codes 8i .. 8i+3
-            const uint32_t c1 = __builtin_amdgcn_perm(odd, even, 0x07030602u);  // codes 8i+4 .. 8i+7
-            lookup4<4>(c0, t, out[4 * i], out[4 * i + 1]);
-            lookup4<4>(c1, t, out[4 * i + 2], out[4 * i + 3]);
-        }
+        const uint32_t x = w[g];
+        ce = x & 0x07070707u;
+        co = (x >> 4) & 0x07070707u;
+        se = ((x >> 1) & 0x04040404u) | 0x03020100u;
+        so = ((x >> 5) & 0x04040404u) | 0x03020100u;
     } else if constexpr (BITS == 2) {
-#pragma unroll
-        for (int g = 0; g < 8; ++g) {
-            const uint32_t x = w[g >> 2] >> (8 * (g & 3));
-            const uint32_t c4 = (x & 3u) | (((x >> 2) & 3u) << 8) | (((x >> 4) & 3u) << 16) | (((x >> 6) & 3u) << 24);
-            lookup4<2>(c4, t, out[2 * g], out[2 * g + 1]);
-        }
+        const uint32_t x = w[g >> 1] >> (16 * (g & 1));      // 16 bits, code j at bits 2j
+        const uint32_t e = x & 0x3333u, o = (x >> 2) & 0x3333u;  // nibble i holds k2i (k2i+1)
+        ce = __builtin_amdgcn_perm(e >> 4, e, 0x05010400u) & 0x03030303u;
+        co = __builtin_amdgcn_perm(o >> 4, o, 0x05010400u) & 0x03030303u;
     } else {
         static_assert(BITS == 3, "bits");
-        const uint64_t lo64 = (uint64_t)w[0] | ((uint64_t)w[1] << 32);
-        const uint64_t hi64 = (uint64_t)w[1] | ((uint64_t)w[2] << 32);
-#pragma unroll
-        for (int g = 0; g < 8; ++g) {
-            const int bit = 12 * g;
-            const uint32_t x = bit < 32 ? (uint32_t)(lo64 >> bit) : (uint32_t)(hi64 >> (bit - 32));
-            const uint32_t c4 = (x & 7u) | (((x >> 3) & 7u) << 8) | (((x >> 6) & 7u) << 16) | (((x >> 9) & 7u) << 24);
-            lookup4<3>(c4, t, out[2 * g], out[2 * g + 1]);
-        }
+        const int bit = 24 * g;                               // 24 bits, code j at bits 3j
+        const uint32_t x = bit == 0 ? w[0] : bit == 24 ? (w[0] >> 24) | (w[1] << 8)
+                         : bit == 48 ? (w[1] >> 16) | (w[2] << 16) : w[2] >> 8;
+        ce = (x & 7u) | (((x >> 6) & 7u) << 8) | (((x >> 12) & 7u) << 16) | (((x >> 18) & 7u) << 24);
+        co = ((x >> 3) & 7u) | (((x >> 9) & 7u) << 8) | (((x >> 15) & 7u) << 16) | (((x >> 21) & 7u) << 24);
     }
+    uint32_t lo, hi;
+    lookup_bytes<BITS>(ce, se, t, lo, hi);
+    interleave(lo, hi, out[0], out[1]);
+    lookup_bytes<BITS>(co, so, t, lo, hi);
+    interleave(lo, hi, out[2], out[3]);
 }
 
 template <int BITS>
@@ -143,17 +152,18 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
     for (int k0 = 0; k0 < p.K; k0 += BK) {
-        uint32_t wa[4], wb[4], da[16], db[16];
+        uint32_t wa[4], wb[4];
         load_codes32<BA>(asrc + (int64_t)k0 * BA / 8, wa);
         load_codes32<BW>(bsrc + (int64_t)k0 * BW / 8, wb);
-        decode32<BA>(wa, ta, da);
-        decode32<BW>(wb, tw, db);
         uint4* adst = (uint4*)(As + lr * LDS_STRIDE + lh * 32);
         uint4* bdst = (uint4*)(Bs + lr * LDS_STRIDE + lh * 32);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            adst[i] = make_uint4(da[4 * i], da[4 * i + 1], da[4 * i + 2], da[4 * i + 3]);
-            bdst[i] = make_uint4(db[4 * i], db[4 * i + 1], db[4 * i + 2], db[4 * i + 3]);
+        for (int g = 0; g < 4; ++g) {
+            uint32_t da[4], db[4];
+            decode8<BA>(wa, g, ta, da);
+            decode8<BW>(wb, g, tw, db);
+            adst[g] = make_uint4(da[0], da[1], da[2], da[3]);
+            bdst[g] = make_uint4(db[0], db[1], db[2], db[3]);
         }
         __syncthreads();
 #pragma unroll
@@ -191,24 +201,183 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     }
 }
 
+// ------------------------------------------------------------------------------------------
+// Large-problem kernel: 256x256 block tiles, K-step 64, eight waves of 128x64 each.  Every code
+// of a block tile is decoded once per K-step into a double-buffered fp16 tile in LDS (147 KB),
+// which halves the decodes per flop of the 128x128 kernel.  While the matrix cores work on step
+// s, each wave decodes step s+1 into the other stage, a quarter per 16-wide k slice, and the
+// codes of step s+2 are in flight.  Block tiles are visited so that the
+// workgroups resident on one XCD (round-robin dispatch) share A and B panels in that XCD's L2.
+constexpr int BM2 = 256, BN2 = 256, BK2 = 64;
+constexpr int LDS2_STRIDE = BK2 + 8;                  // halves per tile row; 144 B keeps 16-byte
+                                                      // fragment reads of 16 rows conflict-free
+constexpr int LDS2_TILE = BM2 * LDS2_STRIDE;          // halves per operand tile
+constexpr int GROUP_M = 8;                            // block rows per L2 group
+
+template <int BA, int BW>
+__global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, int ntn, int per_xcd) {
+    extern __shared__ __align__(16) _Float16 lds[];  // [stage][A, B][256][72]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 2, wn = wave & 3;
+
+    // XCD-aware tile order: workgroup pid runs on XCD pid % 8; consecutive ids per XCD
+    const int pid = blockIdx.x;
+    const int nid = (pid & 7) * per_xcd + (pid >> 3);
+    const int total = ntm * ntn;
+    if (nid >= total) return;
+    const int in_group = GROUP_M * ntn;
+    const int first_m = (nid / in_group) * GROUP_M;
+    const int gsize = min(ntm - first_m, GROUP_M);
+    const int tm = first_m + (nid % in_group) % gsize;
+    const int tn = (nid % in_group) / gsize;
+    const int64_t m0 = (int64_t)tm * BM2, n0 = (int64_t)tn * BN2;
+
+    const ByteTables ta = make_tables(p.lut_a, 1 << BA);
+    const ByteTables tw = make_tables(p.lut_w, 1 << BW);
+
+    // this thread decodes 32 codes of one A row and 32 codes of one B row per K-step
+    const int lr = tid >> 1, lh = tid & 1;
+    const int64_t arow = min(m0 + lr, p.M - 1), brow = min(n0 + lr, p.N - 1);
+    const uint8_t* asrc = p.xc + arow * ((int64_t)p.K * BA / 8) + lh * 4 * BA;
+    const uint8_t* bsrc = p.wc + brow * ((int64_t)p.K * BW / 8) + lh * 4 * BW;
+
+    floatx16 acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    const int nk = p.K / BK2;
+    const int64_t astep = BK2 * BA / 8, bstep = BK2 * BW / 8;
+    _Float16* const a_dst0 = lds + lr * LDS2_STRIDE + lh * 32;  // this thread's decode slots, stage 0
+    const _Float16* const a_frag0 = lds + (wm * 128 + (lane & 31)) * LDS2_STRIDE + (lane >> 5) * 8;
+    const _Float16* const b_frag0 = lds + LDS2_TILE + (wn * 64 + (lane & 31)) * LDS2_STRIDE + (lane >> 5) * 8;
+    constexpr int STAGE = 2 * LDS2_TILE;
+
+    uint32_t wa[4], wb[4];
+    load_codes32<BA>(asrc, wa);
+    load_codes32<BW>(bsrc, wb);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        uint32_t da[4], db[4];
+        decode8<BA>(wa, g, ta, da);
+        decode8<BW>(wb, g, tw, db);
+        *(uint4*)(a_dst0 + 8 * g) = make_uint4(da[0], da[1], da[2], da[3]);
+        *(uint4*)(a_dst0 + LDS2_TILE + 8 * g) = make_uint4(db[0], db[1], db[2], db[3]);
+    }
+    {
+        const int64_t s1 = nk > 1 ? 1 : 0;
+        load_codes32<BA>(asrc + s1 * astep, wa);
+        load_codes32<BW>(bsrc + s1 * bstep, wb);
+    }
+    __syncthreads();
+
+    for (int s = 0; s < nk; ++s) {
+        // codes two steps ahead (the last steps re-load the final step; they are never used)
+        const int64_t s2 = min(s + 2, nk - 1);
+        uint32_t na[4], nb[4];
+        load_codes32<BA>(asrc + s2 * astep, na);
+        load_codes32<BW>(bsrc + s2 * bstep, nb);
+
+        const int cur = (s & 1) * STAGE, nxt = STAGE - cur;
+        half8 a[2][4], b[2][2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[0][i] = *(const half8*)(a_frag0 + cur + i * 32 * LDS2_STRIDE);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[0][j] = *(const half8*)(b_frag0 + cur + j * 32 * LDS2_STRIDE);
+#pragma unroll
+        for (int kk = 0; kk < BK2 / 16; ++kk) {
+            const int f = kk & 1;
+            if (kk + 1 < BK2 / 16) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    a[f ^ 1][i] = *(const half8*)(a_frag0 + cur + i * 32 * LDS2_STRIDE + (kk + 1) * 16);
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    b[f ^ 1][j] = *(const half8*)(b_frag0 + cur + j * 32 * LDS2_STRIDE + (kk + 1) * 16);
+            }
+            // decode one group of the next step's codes into the other stage (it was last read
+            // before the previous barrier); on the final step this refills a stage nobody reads
+            {
+                uint32_t da[4], db[4];
+                decode8<BA>(wa, kk, ta, da);
+                decode8<BW>(wb, kk, tw, db);
+                *(uint4*)(a_dst0 + nxt + 8 * kk) = make_uint4(da[0], da[1], da[2], da[3]);
+                *(uint4*)(a_dst0 + nxt + LDS2_TILE + 8 * kk) = make_uint4(db[0], db[1], db[2], db[3]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[f][i], b[f][j], acc[i][j], 0, 0, 0);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            wa[q] = na[q];
+            wb[q] = nb[q];
+        }
+        __syncthreads();
+    }
+
+    // epilogue: element e of a 32x32 accumulator tile sits at row 8*(e/4) + 4*(lane/32) + e%4, col lane%32
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
+        if (col >= p.N) continue;
+        const float rw = bf16_to_f32(p.wn[col]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int64_t row = m0 + wm * 128 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+                if (row < p.M) p.Y[row * p.ldy + col] = acc[i][j][e] * p.xn[row] * rw;
+            }
+        }
+    }
+}
+
+template <int BA, int BW>
+hipError_t launch_big(const GemmParams& p, hipStream_t stream) {
+    static bool attr = false;
+    const size_t smem = (size_t)2 * 2 * LDS2_TILE * sizeof(_Float16);
+    if (!attr) {
+        hipError_t e = hipFuncSetAttribute((const void*)lut_gemm_big<BA, BW>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)smem);
+        if (e != hipSuccess) return e;
+        attr = true;
+    }
+    const int ntm = (int)((p.M + BM2 - 1) / BM2), ntn = (int)((p.N + BN2 - 1) / BN2);
+    const int per_xcd = (ntm * ntn + 7) / 8;
+    hipLaunchKernelGGL((lut_gemm_big<BA, BW>), dim3(per_xcd * 8), dim3(512), smem, stream, p, ntm, ntn, per_xcd);
+    return hipGetLastError();
+}
+
+template <int BA, int BW>
+hipError_t launch_one(const GemmParams& p, hipStream_t stream, int cus) {
+    // the large kernel needs enough 256x256 tiles to keep every compute unit busy
+    const int64_t tiles = ((p.M + BM2 - 1) / BM2) * ((p.N + BN2 - 1) / BN2);
+    if (tiles >= 2 * (int64_t)cus) return launch_big<BA, BW>(p, stream);
+    dim3 grid((unsigned)((p.N + BN - 1) / BN), (unsigned)((p.M + BM - 1) / BM));
+    hipLaunchKernelGGL((lut_gemm_kernel<BA, BW>), grid, dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
 }  // namespace
 
-hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, hipStream_t stream) {
-    dim3 grid((unsigned)((p.N + BN - 1) / BN), (unsigned)((p.M + BM - 1) / BM));
-#define ORBIT_GEMM(A, W) hipLaunchKernelGGL((lut_gemm_kernel<A, W>), grid, dim3(256), 0, stream, p)
+hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, int cus, hipStream_t stream) {
     switch (ba * 8 + bw) {
-        case 2 * 8 + 2: ORBIT_GEMM(2, 2); break;
-        case 2 * 8 + 3: ORBIT_GEMM(2, 3); break;
-        case 2 * 8 + 4: ORBIT_GEMM(2, 4); break;
-        case 3 * 8 + 2: ORBIT_GEMM(3, 2); break;
-        case 3 * 8 + 3: ORBIT_GEMM(3, 3); break;
-        case 3 * 8 + 4: ORBIT_GEMM(3, 4); break;
-        case 4 * 8 + 2: ORBIT_GEMM(4, 2); break;
-        case 4 * 8 + 3: ORBIT_GEMM(4, 3); break;
-        default: ORBIT_GEMM(4, 4); break;
+        case 2 * 8 + 2: return launch_one<2, 2>(p, stream, cus);
+        case 2 * 8 + 3: return launch_one<2, 3>(p, stream, cus);
+        case 2 * 8 + 4: return launch_one<2, 4>(p, stream, cus);
+        case 3 * 8 + 2: return launch_one<3, 2>(p, stream, cus);
+        case 3 * 8 + 3: return launch_one<3, 3>(p, stream, cus);
+        case 3 * 8 + 4: return launch_one<3, 4>(p, stream, cus);
+        case 4 * 8 + 2: return launch_one<4, 2>(p, stream, cus);
+        case 4 * 8 + 3: return launch_one<4, 3>(p, stream, cus);
+        default: return launch_one<4, 4>(p, stream, cus);
     }
-#undef ORBIT_GEMM
-    return hipGetLastError();
 }
 
 }  // namespace orbit

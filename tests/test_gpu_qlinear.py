@@ -46,6 +46,21 @@ def test_random_codes(M, N, K, ba, bw):
     assert err <= GEMM_REL_F
 
 
+# shapes with at least 512 tiles of 256x256 run the large-tile kernel; these cover its ragged
+# edges in M and N, a single K-step and an odd number of K-steps
+@pytest.mark.parametrize("M,N,K", [(4133, 8061, 64), (4133, 8061, 192), (8197, 4099, 1024)])
+@pytest.mark.parametrize("ba,bw", [(4, 4), (4, 3), (2, 2), (3, 4)])
+def test_random_codes_large_tiles(M, N, K, ba, bw):
+    xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
+    Y = _gpu(xc, xs, wc, wr, ba, bw, K)
+    ref = qlinear_oracle_fp16(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
+    err = rel_frobenius(Y, ref)
+    worst_row = float(np.max(np.linalg.norm(Y - ref, axis=1) / np.maximum(np.linalg.norm(ref, axis=1), 1e-300)))
+    log_stats(f"gemm large-tile M={M} N={N} K={K} W{bw}A{ba}", rel_f=err, worst_row_rel=worst_row)
+    assert err <= GEMM_REL_F
+    assert worst_row <= GEMM_REL_F
+
+
 def test_constant_codes_closed_form():
     M, N, K = 70, 200, 1024
     cba, cbw = oq.lloydmax_codebook(4, K), oq.lloydmax_codebook(3, K)
