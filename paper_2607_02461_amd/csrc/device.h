@@ -38,6 +38,7 @@ struct GemmParams {
     float* Y;              // [M][ldy]
     int64_t M, N, ldy;
     int K;
+    int vec4;              // Y and ldy allow 16-byte row stores; wn allows 8-byte loads
     uint16_t lut_a[16];    // fp16 levels (2^ba used)
     uint16_t lut_w[16];    // fp16 levels (2^bw used)
 };

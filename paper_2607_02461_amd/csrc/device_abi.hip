@@ -222,6 +222,14 @@ orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const fl
     g.N = N;
     g.ldy = ldy;
     g.K = (int)K;
+    g.vec4 = aligned(Y, 16) && ldy % 4 == 0 && aligned(w_norm, 8);
+    for (const orbit_codebook_s* cb : {cb_a, cb_w}) {
+        // the 4-bit decoder reads the positive half and mirrors it
+        if (cb->bits != 4) continue;
+        for (int c = 0; c < 8; ++c)
+            if (cb->lut_f16[15 - c] != (uint16_t)(cb->lut_f16[c] ^ 0x8000u))
+                return fail(ORBIT_EINTERNAL, "orbit_qlinear: 4-bit fp16 levels are not antisymmetric");
+    }
     for (int j = 0; j < 16; ++j) {
         g.lut_a[j] = j < (1 << cb_a->bits) ? cb_a->lut_f16[j] : 0;
         g.lut_w[j] = j < (1 << cb_w->bits) ? cb_w->lut_f16[j] : 0;

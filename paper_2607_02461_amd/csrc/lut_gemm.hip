@@ -25,18 +25,24 @@ constexpr int BM = 128, BN = 128, BK = 64;
 constexpr int LDS_STRIDE = BK + 8;  // halves per tile row (padding against bank conflicts)
 
 struct ByteTables {
-    uint32_t lo[4], hi[4];  // byte e of lo[e/4] (hi[e/4]) is the low (high) byte of level e
+    uint32_t lo[2], hi[2];  // byte e of lo[e/4] (hi[e/4]) is the low (high) byte of table entry e
 };
 
-__device__ __forceinline__ ByteTables make_tables(const uint16_t* lut, int n) {
+// Tables of at most eight levels hold every level.  The 4-bit table holds the positive half
+// L[8..15] only: the codebook is antisymmetric (L[15-c] = -L[c], Sec. 3's symmetric marginal),
+// so a code below 8 reads the mirrored entry and sets the fp16 sign bit.  The host checks the
+// antisymmetry bit for bit before launching.
+template <int BITS>
+__device__ __forceinline__ ByteTables make_tables(const uint16_t* lut) {
+    constexpr int n = BITS == 4 ? 8 : 1 << BITS, first = BITS == 4 ? 8 : 0;
     ByteTables t;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < 2; ++w) {
         uint32_t lo = 0, hi = 0;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
             const int e = 4 * w + b;
-            const uint32_t v = e < n ? lut[e] : 0u;
+            const uint32_t v = e < n ? lut[first + e] : 0u;
             lo |= (v & 0xFFu) << (8 * b);
             hi |= (v >> 8) << (8 * b);
         }
@@ -51,25 +57,10 @@ __device__ __forceinline__ ByteTables make_tables(const uint16_t* lut, int n) {
 // for every bit width, so every MFMA still contracts matching k; the order is the one the 4-bit
 // decoder produces without any byte shuffling (even and odd nibbles of a code word).
 
-// Four 3-bit level indices (one per byte of sel) with a fourth bit per byte in hi8 (bit 2 of each
-// byte of s4, already placed) -> fp16 low and high bytes; for tables of at most eight levels the
-// combine step is skipped.
-template <int BITS>
-__device__ __forceinline__ void lookup_bytes(uint32_t sel, uint32_t s4, const ByteTables& t, uint32_t& lo,
-                                             uint32_t& hi) {
-    if constexpr (BITS <= 3) {
-        lo = __builtin_amdgcn_perm(t.lo[1], t.lo[0], sel);
-        hi = __builtin_amdgcn_perm(t.hi[1], t.hi[0], sel);
-    } else {
-        // levels 0..7 and 8..15 looked up separately, then byte i taken from the second table
-        // when that code's top bit is set (s4 byte i = i + 4 * bit)
-        const uint32_t lo0 = __builtin_amdgcn_perm(t.lo[1], t.lo[0], sel);
-        const uint32_t lo1 = __builtin_amdgcn_perm(t.lo[3], t.lo[2], sel);
-        const uint32_t hi0 = __builtin_amdgcn_perm(t.hi[1], t.hi[0], sel);
-        const uint32_t hi1 = __builtin_amdgcn_perm(t.hi[3], t.hi[2], sel);
-        lo = __builtin_amdgcn_perm(lo1, lo0, s4);
-        hi = __builtin_amdgcn_perm(hi1, hi0, s4);
-    }
+// Four table indices (one per byte of sel, each below 8) -> fp16 low and high bytes.
+__device__ __forceinline__ void lookup_bytes(uint32_t sel, const ByteTables& t, uint32_t& lo, uint32_t& hi) {
+    lo = __builtin_amdgcn_perm(t.lo[1], t.lo[0], sel);
+    hi = __builtin_amdgcn_perm(t.hi[1], t.hi[0], sel);
 }
 
 // low/high byte words of four values -> two fp16x2 words (values 0,1 and 2,3)
@@ -78,19 +69,12 @@ __device__ __forceinline__ void interleave(uint32_t lo, uint32_t hi, uint32_t& d
     d1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);  // [lo2 hi2 lo3 hi3]
 }
 
-// Group g (codes 8g .. 8g+7) of 32 packed codes (4*BITS bytes, LSB-first) -> four fp16x2 words
-// in canonical slot order.
+// 2- and 3-bit groups: every level is in the table
 template <int BITS>
-__device__ __forceinline__ void decode8(const uint32_t (&w)[4], int g, const ByteTables& t, uint32_t (&out)[4]) {
-    uint32_t ce, co;  // codes k0 k2 k4 k6 and k1 k3 k5 k7, one per byte (low BITS bits significant)
-    uint32_t se = 0, so = 0;
-    if constexpr (BITS == 4) {
-        const uint32_t x = w[g];
-        ce = x & 0x07070707u;
-        co = (x >> 4) & 0x07070707u;
-        se = ((x >> 1) & 0x04040404u) | 0x03020100u;
-        so = ((x >> 5) & 0x04040404u) | 0x03020100u;
-    } else if constexpr (BITS == 2) {
+__device__ __forceinline__ void decode8_small(const uint32_t (&w)[4], int g, const ByteTables& t, uint32_t (&out)[4]) {
+    uint32_t lo, hi;
+    uint32_t ce, co;  // codes k0 k2 k4 k6 and k1 k3 k5 k7, one per byte
+    if constexpr (BITS == 2) {
         const uint32_t x = w[g >> 1] >> (16 * (g & 1));      // 16 bits, code j at bits 2j
         const uint32_t e = x & 0x3333u, o = (x >> 2) & 0x3333u;  // nibble i holds k2i (k2i+1)
         ce = __builtin_amdgcn_perm(e >> 4, e, 0x05010400u) & 0x03030303u;
@@ -103,11 +87,31 @@ __device__ __forceinline__ void decode8(const uint32_t (&w)[4], int g, const Byt
         ce = (x & 7u) | (((x >> 6) & 7u) << 8) | (((x >> 12) & 7u) << 16) | (((x >> 18) & 7u) << 24);
         co = ((x >> 3) & 7u) | (((x >> 9) & 7u) << 8) | (((x >> 15) & 7u) << 16) | (((x >> 21) & 7u) << 24);
     }
-    uint32_t lo, hi;
-    lookup_bytes<BITS>(ce, se, t, lo, hi);
+    lookup_bytes(ce, t, lo, hi);
     interleave(lo, hi, out[0], out[1]);
-    lookup_bytes<BITS>(co, so, t, lo, hi);
+    lookup_bytes(co, t, lo, hi);
     interleave(lo, hi, out[2], out[3]);
+}
+
+// Group g (codes 8g .. 8g+7) of 32 packed codes (4*BITS bytes, LSB-first) -> four fp16x2 words
+// in canonical slot order.
+template <int BITS>
+__device__ __forceinline__ void decode8(const uint32_t (&w)[4], int g, const ByteTables& t, uint32_t (&out)[4]) {
+    uint32_t lo, hi;
+    if constexpr (BITS == 4) {
+        // nibble j of x is code k_j; neg has bit 3 of each nibble set where that code is below 8
+        // (a negative level); there the low three bits are mirrored (j -> 7 - j) to index the
+        // positive half, and the sign bit is set on the high byte afterwards
+        const uint32_t x = w[g];
+        const uint32_t neg = ~x & 0x88888888u;
+        const uint32_t idx = x ^ (neg - (neg >> 3));
+        lookup_bytes(idx & 0x07070707u, t, lo, hi);                  // k0 k2 k4 k6
+        interleave(lo, hi | ((neg << 4) & 0x80808080u), out[0], out[1]);
+        lookup_bytes((idx >> 4) & 0x07070707u, t, lo, hi);           // k1 k3 k5 k7
+        interleave(lo, hi | (neg & 0x80808080u), out[2], out[3]);
+    } else {
+        decode8_small<BITS>(w, g, t, out);
+    }
 }
 
 template <int BITS>
@@ -133,8 +137,8 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
-    const ByteTables ta = make_tables(p.lut_a, 1 << BA);
-    const ByteTables tw = make_tables(p.lut_w, 1 << BW);
+    const ByteTables ta = make_tables<BA>(p.lut_a);
+    const ByteTables tw = make_tables<BW>(p.lut_w);
 
     // this thread decodes 32 codes of one A row and 32 codes of one B row per K-step
     const int lr = tid >> 1, lh = tid & 1;
@@ -232,8 +236,8 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     const int tn = (nid % in_group) / gsize;
     const int64_t m0 = (int64_t)tm * BM2, n0 = (int64_t)tn * BN2;
 
-    const ByteTables ta = make_tables(p.lut_a, 1 << BA);
-    const ByteTables tw = make_tables(p.lut_w, 1 << BW);
+    const ByteTables ta = make_tables<BA>(p.lut_a);
+    const ByteTables tw = make_tables<BW>(p.lut_w);
 
     // this thread decodes 32 codes of one A row and 32 codes of one B row per K-step
     const int lr = tid >> 1, lh = tid & 1;
@@ -274,12 +278,17 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     }
     __syncthreads();
 
-    for (int s = 0; s < nk; ++s) {
-        // codes two steps ahead (the last steps re-load the final step; they are never used)
+    // One K-step: MFMAs over stage s&1 while the codes in (ca, cb) - step s+1 - are decoded into
+    // the other stage and the codes of step s+2 load into (na, nb).  The loop below is unrolled
+    // by two so that the code registers swap roles instead of being copied (a copy would wait
+    // for the load).
+    auto kstep = [&](int s, const uint32_t (&ca)[4], const uint32_t (&cb)[4], uint32_t (&na)[4],
+                     uint32_t (&nb)[4]) {
+        // the last steps re-load the final step's codes; they are never used
         const int64_t s2 = min(s + 2, nk - 1);
-        uint32_t na[4], nb[4];
         load_codes32<BA>(asrc + s2 * astep, na);
         load_codes32<BW>(bsrc + s2 * bstep, nb);
+        __builtin_amdgcn_sched_barrier(0);
 
         const int cur = (s & 1) * STAGE, nxt = STAGE - cur;
         half8 a[2][4], b[2][2];
@@ -302,8 +311,8 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
             // before the previous barrier); on the final step this refills a stage nobody reads
             {
                 uint32_t da[4], db[4];
-                decode8<BA>(wa, kk, ta, da);
-                decode8<BW>(wb, kk, tw, db);
+                decode8<BA>(ca, kk, ta, da);
+                decode8<BW>(cb, kk, tw, db);
                 *(uint4*)(a_dst0 + nxt + 8 * kk) = make_uint4(da[0], da[1], da[2], da[3]);
                 *(uint4*)(a_dst0 + nxt + LDS2_TILE + 8 * kk) = make_uint4(db[0], db[1], db[2], db[3]);
             }
@@ -311,28 +320,73 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[f][i], b[f][j], acc[i][j], 0, 0, 0);
-        }
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(b[f][j], a[f][i], acc[i][j], 0, 0, 0);
+            // issue order inside the slice: next fragments first, then each MFMA followed by a
+            // share of the decode, the decoded rows' LDS writes last
+            if (kk + 1 < BK2 / 16) __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            wa[q] = na[q];
-            wb[q] = nb[q];
+            for (int m = 0; m < 8; ++m) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();
-    }
+    };
 
-    // epilogue: element e of a 32x32 accumulator tile sits at row 8*(e/4) + 4*(lane/32) + e%4, col lane%32
+    uint32_t xa[4], xb[4];
+    int s = 0;
+    for (; s + 1 < nk; s += 2) {
+        kstep(s, wa, wb, xa, xb);
+        kstep(s + 1, xa, xb, wa, wb);
+    }
+    if (s < nk) kstep(s, wa, wb, xa, xb);
+
+    // epilogue.  The MFMAs computed the transposed tile, so element e of accumulator (i, j)
+    // belongs to row i*32 + lane%32 and column j*32 + 8*(e/4) + 4*(lane/32) + e%4: each lane
+    // holds runs of four consecutive columns of one row and stores them as one 16-byte vector.
+    const int64_t col0 = n0 + wn * 64 + 4 * (lane >> 5);
+    uint2 rwv[2][4];  // bf16 r' of the lane's columns, four per (j, run)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (col >= p.N) continue;
-        const float rw = bf16_to_f32(p.wn[col]);
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int q = 0; q < 4; ++q) {
+            const int64_t c = col0 + j * 32 + 8 * q;
+            if (c + 3 < p.N && p.vec4) {
+                rwv[j][q] = *(const uint2*)(p.wn + c);
+            } else {
+                uint16_t v[4];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int64_t row = m0 + wm * 128 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                if (row < p.M) p.Y[row * p.ldy + col] = acc[i][j][e] * p.xn[row] * rw;
+                for (int r = 0; r < 4; ++r) v[r] = c + r < p.N ? p.wn[c + r] : (uint16_t)0;
+                rwv[j][q] = make_uint2(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16));
+            }
+        }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t row = m0 + wm * 128 + i * 32 + (lane & 31);
+        if (row >= p.M) continue;
+        const float xs = p.xn[row];
+        float* yrow = p.Y + row * p.ldy;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int64_t c = col0 + j * 32 + 8 * q;
+                const uint2 rw = rwv[j][q];
+                float4 v;
+                v.x = acc[i][j][4 * q + 0] * xs * __uint_as_float(rw.x << 16);
+                v.y = acc[i][j][4 * q + 1] * xs * __uint_as_float(rw.x & 0xFFFF0000u);
+                v.z = acc[i][j][4 * q + 2] * xs * __uint_as_float(rw.y << 16);
+                v.w = acc[i][j][4 * q + 3] * xs * __uint_as_float(rw.y & 0xFFFF0000u);
+                if (c + 3 < p.N && p.vec4) {
+                    *(float4*)(yrow + c) = v;
+                } else {
+                    if (c + 0 < p.N) yrow[c + 0] = v.x;
+                    if (c + 1 < p.N) yrow[c + 1] = v.y;
+                    if (c + 2 < p.N) yrow[c + 2] = v.z;
+                    if (c + 3 < p.N) yrow[c + 3] = v.w;
+                }
             }
         }
     }
