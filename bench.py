@@ -36,11 +36,24 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c4_video_mlp_w4a4", choices=["c4_video_mlp_w4a4", "c1_single_w4a4"])
-    ap.add_argument("--cpu-baseline-rows", type=int, default=2048,
+    ap.add_argument("--cpu-baseline-rows", type=int, default=12288,
                     help="token rows of the oracle's timed CPU sample (0 disables it)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one plain device-to-device copy of this many MiB before the step, so that a "
+                         "counter profile of this run holds a kernel of known traffic to scale by")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-kernel HBM bytes measured with rocprofv3 counters (optional)")
     return ap.parse_args()
+
+
+def source_digest():
+    """Digest of the kernel sources; traffic counters taken from other sources are not used."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("rpbh_quantize.hip", "lut_gemm.hip"):
+        with open(os.path.join(ROOT, "paper_2607_02461_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def quant_bytes(M, K, bits):
@@ -109,6 +122,14 @@ def main():
     weight_pass_ms = ws.elapsed_time(we) / wp_reps
     weight_bytes = sum(L["lin"].N * (2 * L["lin"].K + L["lin"].K * L["lin"].bw // 8 + 2) for L in layers)
 
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     # ---- the step --------------------------------------------------------------------------
     nl = len(layers)
 
@@ -159,7 +180,7 @@ def main():
     if os.path.exists(args.traffic):
         try:
             t = json.load(open(args.traffic))
-            if t.get("workload") == wl.name:
+            if t.get("workload") == wl.name and t.get("source_digest") == source_digest():
                 traffic = t
         except (OSError, ValueError):
             traffic = None
@@ -167,7 +188,7 @@ def main():
     gemm_launch_flops = float(flops.mean())
     gemm_avg_ms = float(gemm_ms.mean())
     roofline = {
-        "kernel": "lut_gemm_kernel<4,4>" if all(L["lin"].ba == 4 and L["lin"].bw == 4 for L in layers) else "lut_gemm_kernel",
+        "kernel": "lut_gemm_big" if wl is workloads.C4 else "lut_gemm_kernel",
         "bound": "mfma",
         "achieved": gemm_launch_flops / (gemm_avg_ms * 1e-3) / 1e12,
         "peak": FP16_MFMA_PEAK_TFLOPS,

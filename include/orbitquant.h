@@ -133,14 +133,16 @@ void lloydmax_codebook_destroy(orbit_codebook c);
  *   N, K    rows and input dimension; N >= 0
  *   ldw     row stride of W in elements, >= K and a multiple of 8
  *   eps     guard added to the norm before dividing (1e-10 in the paper; a zero row gives
- *           r' = 0 and the middle code 2^(b-1) everywhere)
+ *           r' = 0 and the middle code 2^(b-1) everywhere).  Finite and >= 0; the kernel
+ *           floors r' + eps at 1e-30, which only matters for eps below that and rows whose
+ *           norm is smaller still
  *   w_codes device, uint8 [N][K*b_w/8], packed as described above
  *   w_norm  device, bf16 [N]
  *   stream  hipStream_t
  *
  * Pointers: W and w_codes 16-byte aligned, w_norm 2-byte aligned.
  * Errors: ORBIT_EINVAL (null pointer, K mismatch, ldw, alignment); ORBIT_EUNSUPPORTED
- * (h != 128, K > 32768 or bits outside 2..4); ORBIT_EHIP.  N = 0 returns at once.
+ * (h != 128, K > 16384 or bits outside 2..4); ORBIT_EHIP.  N = 0 returns at once.
  */
 orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const uint16_t* W, int64_t N,
                                       int64_t K, int64_t ldw, float eps, uint8_t* w_codes,
@@ -178,7 +180,10 @@ orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t
  *   K                       input dimension; cb_a.d == cb_w.d == K, K a multiple of 64
  *   Y                       device, fp32 [M][ldy], ldy >= N
  *
- * Pointers: codes 16-byte aligned, x_norm 4-byte, w_norm 2-byte, Y 4-byte aligned.
+ * Pointers: codes 16-byte aligned, x_norm 4-byte, w_norm 2-byte, Y 4-byte aligned (Y 16-byte
+ * aligned with ldy % 4 == 0 and w_norm 8-byte aligned enable vector stores; other layouts are
+ * handled element-wise).  The 4-bit decoder relies on the codebook's exact antisymmetry in
+ * fp16 (L[15-c] = -L[c]), which lloydmax_codebook guarantees; ORBIT_EINTERNAL otherwise.
  * Errors: ORBIT_EINVAL (null pointer, dimension mismatch, ldy < N); ORBIT_EUNSUPPORTED
  * (bits outside 2..4, K not a multiple of 64); ORBIT_EHIP.  M = 0 or N = 0 returns at once.
  */

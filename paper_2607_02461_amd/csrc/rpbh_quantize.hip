@@ -24,10 +24,12 @@
 //                v_fmac_f32_dpp computing own + sign*partner.  That leaves the upper lane of each
 //                pair holding the negated output; the sign is fixed per lane,
 //                sigma = (-1)^popcount(q), and is folded into the per-row encoder scale;
-//   encode       t = fma(z, a, c) maps the coordinate to cells of a lookup table in LDS whose cells
-//                are narrower than the smallest threshold gap; one 8-byte read gives the cell's base
-//                code and its threshold (if any), so code = base + (t >= threshold);
-//   pack         one shift-or; 32 codes leave as one 4*b-byte vector store per lane.
+//   encode       t = fma(z, a, c) maps the coordinate to cells of a table in LDS whose cells are
+//                narrower than the smallest gap between thresholds; with the cell's bias b,
+//                y = fma(t, 0.5, b) lies within 0.25 of the code away from the cell's threshold
+//                (if it has one) and crosses code + 0.5 exactly at it;
+//   pack         v_cvt_pk_u8_f32 rounds y to the code and inserts it as one byte of a word;
+//                a few shift-ors close the gaps, and 32 codes leave as one 4*b-byte vector store.
 // The row's squared norm is reduced deterministically: quad DPP sums, per-block partials in LDS,
 // then one wave per row.
 #include <hip/hip_runtime.h>
@@ -302,7 +304,8 @@ struct Quantizer {
 
         // u = z / (s + eps) with z = z_unnormalised / sqrt(128); t = u / w + center is the cell
         // coordinate and round(0.5 t + bias[cell]) the code
-        const float a = sigma * p.enc_inv_w / ((s + p.eps) * 11.313708498984761f);
+        // (the floor keeps t finite, so the table index stays in range, for any eps >= 0)
+        const float a = sigma * p.enc_inv_w / (fmaxf(s + p.eps, 1e-30f) * 11.313708498984761f);
         const float c = p.enc_center;
         const float* tab = (const float*)(smem + kEncOff);
         float y[32];
