@@ -210,6 +210,25 @@ def main():
         "algorithmic_bytes_per_launch": [float(v) for v in qbytes],
     }
 
+    # NEXT row: the activation quantizer with the paper's block-size rule (largest power of two
+    # dividing d: 1024 for 5120, 512 for 13824), same inputs, timed alone
+    paper_h = {}
+    for L in layers:
+        lin = L["lin"]
+        plan_p = oq.rpbh_plan(lin.K, 0, wl.plan_seed)
+        for _ in range(2):
+            oq.rpbh_quantize_act(plan_p, L["cba"], L["X"], 1e-10, L["xc"], L["xn"])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(10):
+            oq.rpbh_quantize_act(plan_p, L["cba"], L["X"], 1e-10, L["xc"], L["xn"])
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 10
+        qb = quant_bytes(lin.M, lin.K, lin.ba)
+        paper_h[lin.name] = {"h": plan_p.h, "ms": ms, "gbs": qb / (ms * 1e-3) / 1e9,
+                             "frac_of_hbm": qb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
     cpu = None
     if args.cpu_baseline_rows > 0:
         cpu = cpu_baseline(layers, args.cpu_baseline_rows)
@@ -249,6 +268,7 @@ def main():
         },
         "roofline": roofline,
         "roofline_quantizer": roofline_q,
+        "quantizer_paper_block_rule": paper_h,
         "cpu_baseline": cpu,
         "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0)},
     }

@@ -63,7 +63,9 @@ typedef struct orbit_codebook_s* orbit_codebook;
  *
  *   d     input dimension, >= 1
  *   h     Hadamard block size: a power of two dividing d; 0 selects the paper's rule,
- *         the largest power of two dividing d (Sec. 4.4)
+ *         the largest power of two dividing d (Sec. 4.4).  The device kernels implement
+ *         128 <= h <= 4096 (the rule gives 1024 for d = 3072 and 5120, 4096 for 12288 and
+ *         512 for 13824); other sizes are valid plans for the host API only
  *   seed  generator seed.  pi and the signs are drawn from SplitMix64 (Steele, Lea &
  *         Flood 2014) started at state = seed: Fisher-Yates from the identity for
  *         j = d-1 .. 1 with k uniform in [0, j] (draw u until u >= 2^64 mod (j+1), take
@@ -142,7 +144,7 @@ void lloydmax_codebook_destroy(orbit_codebook c);
  *
  * Pointers: W and w_codes 16-byte aligned, w_norm 2-byte aligned.
  * Errors: ORBIT_EINVAL (null pointer, K mismatch, ldw, alignment); ORBIT_EUNSUPPORTED
- * (h != 128, K > 16384 or bits outside 2..4); ORBIT_EHIP.  N = 0 returns at once.
+ * (h outside 128..4096, K > 16384 or bits outside 2..4); ORBIT_EHIP.  N = 0 returns at once.
  */
 orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const uint16_t* W, int64_t N,
                                       int64_t K, int64_t ldw, float eps, uint8_t* w_codes,

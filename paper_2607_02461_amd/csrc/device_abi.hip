@@ -12,8 +12,9 @@ using namespace orbit;
 
 namespace {
 
-constexpr int kQuantH = 128;       // block size implemented by the fused quantizer
+constexpr int kQuantH = 128;       // the fused quantizer's in-register transform (larger h adds stages)
 constexpr int64_t kQuantMaxK = 16384;
+constexpr int kQuantMaxH = 4096;  // block sizes 128 .. 4096 (the FWHT's stages across blocks)
 constexpr int kQuantMaxCells = 2048;  // encoder table cells (LDS budget)
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
@@ -103,7 +104,9 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
                     (long long)cb->d);
     if (!(eps >= 0.0f) || !std::isfinite(eps)) return fail(ORBIT_EINVAL, "%s: eps must be finite and >= 0", who);
     if (ldx < K || ldx % 8 != 0) return fail(ORBIT_EINVAL, "%s: ld=%lld must be >= K and a multiple of 8", who, (long long)ldx);
-    if (p->h != kQuantH) return fail(ORBIT_EUNSUPPORTED, "%s: block size h=%d not implemented (h=128 is)", who, p->h);
+    if (p->h < kQuantH || p->h > kQuantMaxH)
+        return fail(ORBIT_EUNSUPPORTED, "%s: block size h=%d not implemented (powers of two 128..%d are)", who, p->h,
+                    kQuantMaxH);
     if (cb->bits < 2 || cb->bits > 4) return fail(ORBIT_EUNSUPPORTED, "%s: %d-bit codes not implemented (2..4 are)", who, cb->bits);
     if (K > kQuantMaxK) return fail(ORBIT_EUNSUPPORTED, "%s: K=%lld above %lld", who, (long long)K, (long long)kQuantMaxK);
     if ((int64_t)quant_rows_per_group((int)K) * ldx * 2 >= ((int64_t)1 << 31))
@@ -143,7 +146,10 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     q.enc_inv_w = cb->enc.inv_w;
     q.enc_center = cb->enc.center;
     q.one_one = 0x3F803F80u;
-    // two workgroups fit a compute unit (LDS: double row buffer + encoder table)
+    q.outer = 0;
+    while ((kQuantH << q.outer) < p->h) ++q.outer;
+    q.sqrt_h = (float)std::sqrt((double)p->h);
+    // two workgroups fit a compute unit (LDS: row buffer + encoder table + block partials)
     const int grid = (int)std::min<int64_t>(q.ngroups, (int64_t)info.cus * 2);
     hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, grid, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, who);

@@ -30,6 +30,12 @@
 //                (if it has one) and crosses code + 0.5 exactly at it;
 //   pack         v_cvt_pk_u8_f32 rounds y to the code and inserts it as one byte of a word;
 //                a few shift-ors close the gaps, and 32 codes leave as one 4*b-byte vector store.
+// Blocks larger than 128 (h = 128 * 2^m, up to 4096): Sylvester H_h = (H_{2^m} (x) I_128)(I_{2^m} (x)
+// H_128), so after the 128-point transform the remaining m stages pair equal offsets of the 128-blocks
+// of an h-block.  The quads of an h-block are consecutive and aligned, so stage j pairs lanes 4*2^j
+// apart: ds_swizzle (xor 4, 8, 16) or ds_bpermute (xor 32) within a wave, and for h = 4096 an
+// exchange through LDS between two waves.  Each stage again leaves the upper lane's value negated,
+// which the per-lane encoder sign absorbs.
 // The row's squared norm is reduced deterministically: quad DPP sums, per-block partials in LDS,
 // then one wave per row.
 #include <hip/hip_runtime.h>
@@ -51,6 +57,25 @@ __device__ __forceinline__ float quad_perm(float v) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 constexpr int kQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
+
+// z[r] <- z[r] + sgn * z[r] of lane (lane ^ XOR), for XOR in {4, 8, 16, 32}
+// (eight registers at a time, so that the exchanges in flight need few temporaries)
+template <int XOR>
+__device__ __forceinline__ void lane_xor_stage(float (&z)[32], float sgn, int lane) {
+#pragma unroll
+    for (int c = 0; c < 32; c += 8) {
+#pragma unroll
+        for (int r = c; r < c + 8; ++r) {
+            int v;
+            if constexpr (XOR < 32)
+                v = __builtin_amdgcn_ds_swizzle(__float_as_int(z[r]), 0x1F | (XOR << 10));  // lane ^ XOR in 32
+            else
+                v = __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __float_as_int(z[r]));
+            z[r] = fmaf(__int_as_float(v), sgn, z[r]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
 constexpr int kQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
 
 // z[r] <- z[r] + sgn * z[r] of the partner lane, for 16 registers, as fused DPP FMACs.  The compiler
@@ -191,7 +216,7 @@ __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[4
     }
 }
 
-template <int BITS, bool NORM_BF16>
+template <int BITS, bool NORM_BF16, bool OUTER>
 struct Quantizer {
     const QuantParams& p;
     unsigned char* smem;
@@ -277,10 +302,48 @@ struct Quantizer {
         ORBIT_DPP_FMAC16(z, 16, sgn1, "quad_perm:[1,0,3,2]");
         ORBIT_DPP_FMAC16(z, 0, sgn2, "quad_perm:[2,3,0,1]");
         ORBIT_DPP_FMAC16(z, 16, sgn2, "quad_perm:[2,3,0,1]");
+        if constexpr (OUTER) {
+            // stages across the 128-blocks of an h-block; lane bit 2+j of the quad pairs it
+            const int lane = tid & 63, task = tid >> 2;
+            if (p.outer > 0) lane_xor_stage<4>(z, (task & 1) ? -1.f : 1.f, lane);
+            if (p.outer > 1) lane_xor_stage<8>(z, (task & 2) ? -1.f : 1.f, lane);
+            if (p.outer > 2) lane_xor_stage<16>(z, (task & 4) ? -1.f : 1.f, lane);
+            if (p.outer > 3) lane_xor_stage<32>(z, (task & 8) ? -1.f : 1.f, lane);
+        }
         ss += quad_perm<kQuadXor1>(ss);
         ss += quad_perm<kQuadXor2>(ss);
         if (owner && q == 0) part[rg * nb + blk] = ss;
         __syncthreads();
+
+        if constexpr (OUTER) {
+            if (p.outer > 4) {
+                // h = 4096: the last stage pairs lanes 64 apart, in two waves.  The staging buffer
+                // is free once every wave has passed the barrier above (all gathers are done); it
+                // holds half of the lanes' values at a time.
+                float* xb = (float*)smem;
+                const float sgn = (tid & 64) ? -1.f : 1.f;
+#pragma unroll
+                for (int hf = 0; hf < 2; ++hf) {
+                    if (hf) __syncthreads();
+                    float4* dst = (float4*)(xb + tid * 16);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        dst[i] = make_float4(z[16 * hf + 4 * i], z[16 * hf + 4 * i + 1], z[16 * hf + 4 * i + 2],
+                                             z[16 * hf + 4 * i + 3]);
+                    __syncthreads();
+                    const float4* src = (const float4*)(xb + (tid ^ 64) * 16);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float4 v = src[i];
+                        z[16 * hf + 4 * i] = fmaf(v.x, sgn, z[16 * hf + 4 * i]);
+                        z[16 * hf + 4 * i + 1] = fmaf(v.y, sgn, z[16 * hf + 4 * i + 1]);
+                        z[16 * hf + 4 * i + 2] = fmaf(v.z, sgn, z[16 * hf + 4 * i + 2]);
+                        z[16 * hf + 4 * i + 3] = fmaf(v.w, sgn, z[16 * hf + 4 * i + 3]);
+                    }
+                }
+                __syncthreads();  // every read of the exchange is done before the buffer is refilled
+            }
+        }
 
         // Row totals: each wave reduces the block partials of the rows its lanes hold (the same
         // fixed-order sum in every wave), so no second barrier is needed.  The lane holding block 0
@@ -302,10 +365,10 @@ struct Quantizer {
                 ((float*)p.norm)[row0 + rg] = s;
         }
 
-        // u = z / (s + eps) with z = z_unnormalised / sqrt(128); t = u / w + center is the cell
+        // u = z / (s + eps) with z = z_unnormalised / sqrt(h); t = u / w + center is the cell
         // coordinate and round(0.5 t + bias[cell]) the code
         // (the floor keeps t finite, so the table index stays in range, for any eps >= 0)
-        const float a = sigma * p.enc_inv_w / (fmaxf(s + p.eps, 1e-30f) * 11.313708498984761f);
+        const float a = sigma * p.enc_inv_w / (fmaxf(s + p.eps, 1e-30f) * p.sqrt_h);
         const float c = p.enc_center;
         const float* tab = (const float*)(smem + kEncOff);
         float y[32];
@@ -325,10 +388,10 @@ struct Quantizer {
     }
 };
 
-template <int BITS, bool NORM_BF16>
+template <int BITS, bool NORM_BF16, bool OUTER>
 __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    Quantizer<BITS, NORM_BF16> Q{p, smem};
+    Quantizer<BITS, NORM_BF16, OUTER> Q{p, smem};
     Q.tid = threadIdx.x;
     Q.T = blockDim.x;
     const int task = Q.tid >> 2;
@@ -340,6 +403,11 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
     Q.blk = task - Q.rg * p.nb;
     Q.cpr = p.K >> 3;
     Q.sigma = ((Q.q & 1) ? -1.f : 1.f) * ((Q.q & 2) ? -1.f : 1.f);
+    if constexpr (OUTER) {
+        // one more negation per stage across blocks in which this lane is the upper partner
+        for (int j = 0; j < p.outer; ++j)
+            if ((task >> j) & 1) Q.sigma = -Q.sigma;
+    }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int c = Q.tid + k * Q.T, r = c / Q.cpr;
@@ -371,12 +439,12 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
     for (int g = blockIdx.x; g < p.ngroups; g += gridDim.x) Q.iteration(g);
 }
 
-template <int BITS, bool NB>
+template <int BITS, bool NB, bool OUTER>
 void set_smem_limit() {
     static bool done = false;
     if (!done) {
-        (void)hipFuncSetAttribute((const void*)rpbh_quantize_kernel<BITS, NB>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            160 * 1024);
+        (void)hipFuncSetAttribute((const void*)rpbh_quantize_kernel<BITS, NB, OUTER>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
         done = true;
     }
 }
@@ -396,20 +464,25 @@ int quant_rows_per_group(int K) {
 hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, int grid, hipStream_t stream) {
     const int threads = ((p.R * p.nb * 4 + 63) / 64) * 64;
     const size_t smem = quant_smem_bytes(p.K, p.R, p.ncell);
-#define ORBIT_LAUNCH(B, NB)                                                                        \
+#define ORBIT_LAUNCH(B, NB, OU)                                                                    \
     do {                                                                                           \
-        set_smem_limit<B, NB>();                                                                   \
-        hipLaunchKernelGGL((rpbh_quantize_kernel<B, NB>), dim3(grid), dim3(threads), smem, stream, p); \
+        set_smem_limit<B, NB, OU>();                                                               \
+        hipLaunchKernelGGL((rpbh_quantize_kernel<B, NB, OU>), dim3(grid), dim3(threads), smem, stream, p); \
+    } while (0)
+#define ORBIT_LAUNCH_BITS(NB, OU)                                                                  \
+    do {                                                                                           \
+        if (bits == 2) ORBIT_LAUNCH(2, NB, OU);                                                    \
+        else if (bits == 3) ORBIT_LAUNCH(3, NB, OU);                                               \
+        else ORBIT_LAUNCH(4, NB, OU);                                                              \
     } while (0)
     if (norm_bf16) {
-        if (bits == 2) ORBIT_LAUNCH(2, true);
-        else if (bits == 3) ORBIT_LAUNCH(3, true);
-        else ORBIT_LAUNCH(4, true);
+        if (p.outer > 0) ORBIT_LAUNCH_BITS(true, true);
+        else ORBIT_LAUNCH_BITS(true, false);
     } else {
-        if (bits == 2) ORBIT_LAUNCH(2, false);
-        else if (bits == 3) ORBIT_LAUNCH(3, false);
-        else ORBIT_LAUNCH(4, false);
+        if (p.outer > 0) ORBIT_LAUNCH_BITS(false, true);
+        else ORBIT_LAUNCH_BITS(false, false);
     }
+#undef ORBIT_LAUNCH_BITS
 #undef ORBIT_LAUNCH
     return hipGetLastError();
 }

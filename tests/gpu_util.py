@@ -30,9 +30,9 @@ def to_f64(t: torch.Tensor) -> np.ndarray:
 
 
 def quantize_gpu(X: torch.Tensor, bits: int, seed: int = 0, weights: bool = False, eps: float = 1e-10,
-                 plan=None):
+                 plan=None, h: int = 128):
     K = X.shape[1]
-    plan = plan or oq.rpbh_plan(K, 128, seed)
+    plan = plan or oq.rpbh_plan(K, h, seed)
     cb = oq.lloydmax_codebook(bits, K)
     if weights:
         codes, norms = oq.quantize_weights_offline(plan, cb, X, eps)
@@ -43,13 +43,14 @@ def quantize_gpu(X: torch.Tensor, bits: int, seed: int = 0, weights: bool = Fals
 
 
 def compare_quantizer(name, X: torch.Tensor, bits: int, seed: int = 0, weights: bool = False,
-                      eps: float = 1e-10, rows=None, oplan=None, plan=None):
-    """Quantize all rows of X on the GPU; compare `rows` (default all) with the oracle."""
+                      eps: float = 1e-10, rows=None, oplan=None, plan=None, h: int = 128):
+    """Quantize all rows of X on the GPU (block size h); compare `rows` (default all) with the
+    oracle."""
     M, K = X.shape
-    codes, norms = quantize_gpu(X, bits, seed, weights, eps, plan=plan)
+    codes, norms = quantize_gpu(X, bits, seed, weights, eps, plan=plan, h=h)
     sel = np.arange(M) if rows is None else np.asarray(rows)
     Xs = to_f64(X[torch.as_tensor(sel, device=X.device)]) if rows is not None else to_f64(X)
-    oplan = oplan or oracle.rpbh_plan(K, 128, seed)
+    oplan = oplan or oracle.rpbh_plan(K, h, seed)
     ocb = oracle.lloydmax_codebook(bits, K)
     if weights:
         oc, on, U = oracle.quantize_weights(Xs, oplan, ocb, eps)
@@ -69,7 +70,7 @@ def compare_quantizer(name, X: torch.Tensor, bits: int, seed: int = 0, weights: 
         gn = norms.cpu().numpy().astype(np.float64)[sel]
         norm_err = float(np.max(np.abs(gn - on) / np.maximum(on, 1e-30))) if len(on) else 0.0
         norm_ok = norm_err <= 1e-5 or bool(np.all(np.abs(gn - on) <= 1e-30))
-    log_stats(name, M=M, K=K, bits=bits, weights=weights, rows_checked=len(sel), elements=int(gc.size),
+    log_stats(name, M=M, K=K, h=oplan.h, bits=bits, weights=weights, rows_checked=len(sel), elements=int(gc.size),
               near_ties=int(near.sum()), near_tie_frac=float(near.mean()) if near.size else 0.0,
               near_tie_mismatches=int(np.sum(mism & near)), mismatches_off_tie=bad,
               norm_err=norm_err)

@@ -32,6 +32,35 @@ def test_small_shapes(K, M, bits, weights):
     compare_quantizer(f"small K={K} M={M}", X, bits, seed=K % 5, weights=weights)
 
 
+# block sizes above 128: the paper's rule (largest power of two dividing d) for the workload
+# dimensions, every size up to 4096 alone, and ragged row counts spanning several groups
+@pytest.mark.parametrize("K,h,M", [(256, 256, 77), (512, 512, 33), (1024, 1024, 129), (2048, 2048, 17),
+                                   (4096, 4096, 9), (3072, 1024, 257), (5120, 1024, 130), (12288, 4096, 7),
+                                   (13824, 512, 5), (8192, 4096, 6), (16384, 4096, 3), (6144, 2048, 11),
+                                   (1536, 512, 40), (2560, 256, 50)])
+@pytest.mark.parametrize("weights", [False, True])
+def test_block_sizes(K, h, M, weights):
+    X = _randn_bf16(M, K, seed=K + h + M, scale=0.5)
+    for bits in (4,) if weights else (2, 3, 4):
+        compare_quantizer(f"block h={h} K={K} M={M}", X, bits, seed=K % 3, weights=weights, h=h)
+
+
+def test_paper_block_rule_c1():
+    # h = 0 selects the paper's rule: 1024 for d = 3072
+    X, W = workloads.c1_inputs(device=DEV)
+    plan = oq.rpbh_plan(3072, 0, 0)
+    assert plan.h == 1024
+    compare_quantizer("c1 act paper h", X, 4, seed=0, plan=plan, h=1024)
+    compare_quantizer("c1 weights paper h", W, 4, seed=0, weights=True, plan=plan, h=1024)
+
+
+def test_block_size_outlier_channels():
+    # outlier channels spread by the permutation across a 4096-block
+    Xq, _, _, _ = workloads.c3_inputs(device=DEV)
+    X = torch.cat([Xq[:64], Xq[:64], Xq[:64], Xq[:64]], dim=1).contiguous()  # K = 12288
+    compare_quantizer("c3-like act h=4096", X, 4, seed=1, h=4096)
+
+
 @pytest.mark.parametrize("seed", [0, 1, 2])
 @pytest.mark.parametrize("bits", [2, 3, 4])
 def test_c1_activations_full(seed, bits):
@@ -62,6 +91,16 @@ def test_c4_down_sampled_rows():
     rows = np.sort(np.random.default_rng(44).choice(X.shape[0], 4096, replace=False))
     rows[-1] = X.shape[0] - 1                     # include the ragged tail
     compare_quantizer("c4 down act sampled", X, 4, seed=0, rows=rows)
+    # and with the paper's block-size rule (512 for d = 13824)
+    compare_quantizer("c4 down act sampled, h=512", X, 4, seed=0, rows=rows, h=512)
+
+
+def test_c4_up_paper_block_rule_sampled_rows():
+    fr, tpf, txt = 21, 30 * 52, 512
+    X = workloads.video_acts(fr * tpf, txt, 5120, 4, fr, workloads.C4.data_seed, 0, device=DEV)
+    rows = np.sort(np.random.default_rng(47).choice(X.shape[0], 4096, replace=False))
+    rows[-1] = X.shape[0] - 1
+    compare_quantizer("c4 up act sampled, h=1024", X, 4, seed=0, rows=rows, h=1024)
 
 
 def test_c4_up_weights_sampled_rows():

@@ -126,6 +126,9 @@ def test_device_calls_validate_before_launch():
     assert st == oq.ORBIT_EUNSUPPORTED
     st, _ = _status(lib.rpbh_quantize_act, p.handle, cb1.handle, fake, 4, 256, 256, 1e-10, fake, fake, null)
     assert st == oq.ORBIT_EUNSUPPORTED
+    p_h8k, cb_8k = oq.rpbh_plan(8192, 8192, 0), oq.lloydmax_codebook(4, 8192)   # above the 4096 limit
+    st, msg = _status(lib.rpbh_quantize_act, p_h8k.handle, cb_8k.handle, fake, 4, 8192, 8192, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EUNSUPPORTED and "h=8192" in msg
     # bad stride, negative rows, bad eps, null pointers, misalignment
     st, _ = _status(lib.rpbh_quantize_act, p.handle, cb4.handle, fake, 4, 256, 100, 1e-10, fake, fake, null)
     assert st == oq.ORBIT_EINVAL
