@@ -229,6 +229,49 @@ def main():
         paper_h[lin.name] = {"h": plan_p.h, "ms": ms, "gbs": qb / (ms * 1e-3) / 1e9,
                              "frac_of_hbm": qb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
 
+    # NEXT row: the rotation classes of the paper's ablation (Table 4), on the up-projection input:
+    # fused quantizer time with RPBH and with Block-RHT (RPBH without the permutation) at h = 128
+    # and at the paper's rule, and the dense-rotation alternative as a bf16 GEMM X Q^T (rotation
+    # only, the cost the structured rotations avoid)
+    L0 = layers[0]
+    K0 = L0["lin"].K
+
+    def time_quant(plan_v, reps=10):
+        for _ in range(2):
+            oq.rpbh_quantize_act(plan_v, L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            oq.rpbh_quantize_act(plan_v, L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    rot = {}
+    for hh in (128, 0):
+        pr = oq.rpbh_plan(K0, hh, wl.plan_seed)
+        _, signs = pr.arrays()
+        pb = oq.rpbh_plan_from_arrays(K0, pr.h, np.arange(K0), signs)
+        rot[f"rpbh_h{pr.h}_ms"] = time_quant(pr)
+        rot[f"block_rht_h{pr.h}_ms"] = time_quant(pb)
+    gq = torch.Generator(device=dev)
+    gq.manual_seed(7)
+    Q, _ = torch.linalg.qr(torch.randn((K0, K0), generator=gq, device=dev, dtype=torch.float32))
+    Qt = Q.t().contiguous().to(torch.bfloat16)
+    del Q
+    Xr = torch.empty((L0["lin"].M, K0), dtype=torch.bfloat16, device=dev)
+    for _ in range(2):
+        torch.matmul(L0["X"], Qt, out=Xr)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        torch.matmul(L0["X"], Qt, out=Xr)
+    e1.record()
+    torch.cuda.synchronize()
+    rot["dense_haar_rotation_gemm_ms"] = e0.elapsed_time(e1) / 5
+    rot["shape"] = f"{L0['lin'].M} x {K0}"
+    del Qt, Xr
+
     cpu = None
     if args.cpu_baseline_rows > 0:
         cpu = cpu_baseline(layers, args.cpu_baseline_rows)
@@ -269,6 +312,7 @@ def main():
         "roofline": roofline,
         "roofline_quantizer": roofline_q,
         "quantizer_paper_block_rule": paper_h,
+        "rotation_classes": rot,
         "cpu_baseline": cpu,
         "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0)},
     }

@@ -152,6 +152,20 @@ def test_plan_from_caller_arrays():
     compare_quantizer("c1 act caller plan", X, 4, plan=plan, oplan=oplan)
 
 
+@pytest.mark.parametrize("K,h", [(3072, 128), (3072, 1024), (4096, 4096)])
+def test_rotation_classes_without_permutation(K, h):
+    # Block-RHT (RPBH without the permutation) and, for h = K = 4096, Full RHT: the same kernel
+    # with an identity gather (the rotation classes of the paper's ablation, Table 4)
+    signs = oq.rpbh_plan(K, h, 0).arrays()[1]
+    ident = np.arange(K)
+    plan = oq.rpbh_plan_from_arrays(K, h, ident, signs)
+    oplan = oracle.Plan(d=K, h=h, perm=ident.astype(np.int64), sign=signs.astype(np.float64))
+    X = _randn_bf16(129, K, seed=K + h)
+    X[:, 5:37] = X[:, 5:37] * 30          # clustered outlier channels
+    for bits in (2, 4):
+        compare_quantizer(f"rotation class identity-pi K={K} h={h}", X, bits, plan=plan, oplan=oplan)
+
+
 def test_strided_rows():
     base = _randn_bf16(40, 3072 + 64, seed=11)
     X = base[:, 32:32 + 3072]            # ldx = 3136, rows start 64 bytes in
