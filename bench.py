@@ -272,6 +272,24 @@ def main():
     rot["shape"] = f"{L0['lin'].M} x {K0}"
     del Qt, Xr
 
+    # NEXT row: the up-projection with the MLP's GELU and a bf16 output fused into the epilogue
+    # (the form that feeds the next quantizer), against the plain fp32 GEMM on the same codes
+    Yb = torch.empty((L0["lin"].M, L0["lin"].N), dtype=torch.bfloat16, device=dev)
+    for _ in range(2):
+        oq.orbit_qlinear_ex(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], gelu=True,
+                            out_dtype=torch.bfloat16, out=Yb)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        oq.orbit_qlinear_ex(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], gelu=True,
+                            out_dtype=torch.bfloat16, out=Yb)
+    e1.record()
+    torch.cuda.synchronize()
+    fused_ms = e0.elapsed_time(e1) / 5
+    fused = {"linear": L0["lin"].name, "epilogue": "GELU(erf) + bf16 output", "ms": fused_ms,
+             "tflops": float(flops[0]) / (fused_ms * 1e-3) / 1e12, "plain_fp32_ms": float(gemm_ms[0])}
+    del Yb
+
     cpu = None
     if args.cpu_baseline_rows > 0:
         cpu = cpu_baseline(layers, args.cpu_baseline_rows)
@@ -313,6 +331,7 @@ def main():
         "roofline_quantizer": roofline_q,
         "quantizer_paper_block_rule": paper_h,
         "rotation_classes": rot,
+        "fused_epilogue": fused,
         "cpu_baseline": cpu,
         "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0)},
     }

@@ -193,6 +193,29 @@ orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const fl
                            orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
                            int64_t K, float* Y, int64_t ldy, void* stream);
 
+/*
+ * orbit_qlinear_ex -- orbit_qlinear with the rest of the layer fused into its epilogue, so the
+ * output can feed the next layer's quantizer directly (the low-bit layer consumed natively, as
+ * the paper's Limitations and Future Work section asks; the DiT MLP's two projections with the
+ * GELU between them, Sec. 5's models):
+ *     Y[n][i] = act(x_norm[n] * w_norm[i] * sum_k L_a[...] * L_w[...] + bias[i])
+ *
+ *   bias       device, bf16 [N], or NULL for none (Eq. (1) itself has no bias)
+ *   act        ORBIT_ACT_NONE, or ORBIT_ACT_GELU: x * Phi(x) with the exact error function
+ *   out_dtype  ORBIT_OUT_F32, or ORBIT_OUT_BF16 (round to nearest even), the input type of
+ *              rpbh_quantize_act
+ *   Y          device, [M][ldy] elements of out_dtype
+ *   other arguments, limits and errors as for orbit_qlinear; ORBIT_EINVAL also for an unknown
+ *   act or out_dtype, and Y must be aligned to its element size (bias to 2 bytes).
+ * With bias = NULL, act = ORBIT_ACT_NONE and out_dtype = ORBIT_OUT_F32 this is orbit_qlinear.
+ */
+enum { ORBIT_ACT_NONE = 0, ORBIT_ACT_GELU = 1 };
+enum { ORBIT_OUT_F32 = 0, ORBIT_OUT_BF16 = 1 };
+orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                              orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
+                              int64_t K, const uint16_t* bias, int32_t act, int32_t out_dtype, void* Y,
+                              int64_t ldy, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -27,12 +27,12 @@ from .plan import SplitMix64, rpbh_plan, Plan
 from .rpbh import rpbh_forward, rpbh_inverse, sylvester_hadamard, fwht_blocks
 from .quantize import (normalize_rows, encode, decode_levels, pack_codes, unpack_codes,
                        quantize_act, quantize_weights, near_tie_mask, bf16_round, fp16_round)
-from .qlinear import qlinear, qlinear_dense_reference
+from .qlinear import layer_epilogue, qlinear, qlinear_dense_reference
 
 EPS_DEFAULT = 1e-10  # Sec. 4.3: the clamp guarding zero-norm (padding) tokens
 
 __all__ = [
-    "marginal_pdf", "marginal_cdf", "marginal_mass", "marginal_partial_moment", "log_norm_const",
+    "marginal_pdf", "marginal_cdf", "marginal_mass", "layer_epilogue", "marginal_partial_moment", "log_norm_const",
     "lloydmax_codebook", "Codebook", "SplitMix64", "rpbh_plan", "Plan",
     "rpbh_forward", "rpbh_inverse", "sylvester_hadamard", "fwht_blocks",
     "normalize_rows", "encode", "decode_levels", "pack_codes", "unpack_codes",

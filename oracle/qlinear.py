@@ -23,3 +23,16 @@ def qlinear(codes_x, s, levels_a, codes_w, r, levels_w) -> np.ndarray:
 def qlinear_dense_reference(X, W) -> np.ndarray:
     """The unquantized layer Y = X W^T (Eq. (1), tokens as rows), fp64."""
     return np.asarray(X, dtype=np.float64) @ np.asarray(W, dtype=np.float64).T
+
+
+def layer_epilogue(Y, bias=None, gelu: bool = False, out_bf16: bool = False) -> np.ndarray:
+    """The rest of a DiT linear after the contraction: + bias, then GELU x*Phi(x) with the exact
+    error function, then (optionally) rounding to BF16 as the next layer's input, all in fp64."""
+    from scipy.special import erf
+    from .quantize import bf16_round
+    Y = np.asarray(Y, dtype=np.float64)
+    if bias is not None:
+        Y = Y + np.asarray(bias, dtype=np.float64)[None, :]
+    if gelu:
+        Y = 0.5 * Y * (1.0 + erf(Y / np.sqrt(2.0)))
+    return bf16_round(Y) if out_bf16 else Y

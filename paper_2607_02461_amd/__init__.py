@@ -43,7 +43,13 @@ SIGNATURES = {
                                          ctypes.c_float, _c_void_p, _c_void_p, _c_void_p]),
     "orbit_qlinear": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
                                      _c_void_p, _i64, _i64, _c_void_p, _i64, _c_void_p]),
+    "orbit_qlinear_ex": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
+                                        _c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _c_void_p, _i64,
+                                        _c_void_p]),
 }
+
+ORBIT_ACT_NONE, ORBIT_ACT_GELU = 0, 1
+ORBIT_OUT_F32, ORBIT_OUT_BF16 = 0, 1
 
 _lib = None
 
@@ -220,6 +226,28 @@ def orbit_qlinear(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor, c
     return out
 
 
+def orbit_qlinear_ex(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor, cb_w: Codebook,
+                     w_codes: torch.Tensor, w_norm: torch.Tensor, bias: torch.Tensor = None, gelu: bool = False,
+                     out_dtype: torch.dtype = torch.float32, out: torch.Tensor = None) -> torch.Tensor:
+    """The quantized layer with bias, GELU and the output type fused into the GEMM's epilogue."""
+    M, N = x_codes.shape[0], w_codes.shape[0]
+    K = cb_a.d
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype, device=x_codes.device)
+    if out.dim() != 2 or out.stride(1) != 1 or out.dtype != out_dtype:
+        raise ValueError("out must be a 2-D tensor of out_dtype with contiguous rows")
+    if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != N or not bias.is_contiguous()):
+        raise ValueError("bias must be a contiguous bf16 vector of N entries")
+    _check("orbit_qlinear_ex", lib().orbit_qlinear_ex(
+        cb_a.handle, _ptr(x_codes), _ptr(x_norm), M, cb_w.handle, _ptr(w_codes), _ptr(w_norm), N, K,
+        _ptr(bias) if bias is not None else None, ORBIT_ACT_GELU if gelu else ORBIT_ACT_NONE,
+        ORBIT_OUT_BF16 if out_dtype == torch.bfloat16 else ORBIT_OUT_F32, _ptr(out), out.stride(0),
+        _stream(x_codes)))
+    return out
+
+
 __all__ = ["rpbh_plan", "rpbh_plan_from_arrays", "lloydmax_codebook", "quantize_weights_offline",
-           "rpbh_quantize_act", "orbit_qlinear", "Plan", "Codebook", "OrbitError", "lib", "LIB_PATH",
+           "rpbh_quantize_act", "orbit_qlinear", "orbit_qlinear_ex", "Plan", "Codebook", "OrbitError", "lib", "LIB_PATH",
            "SIGNATURES", "code_bytes"]

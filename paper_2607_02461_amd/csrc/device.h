@@ -37,10 +37,13 @@ struct GemmParams {
     const float* xn;       // [M]
     const uint8_t* wc;     // [N][K*bw/8]
     const uint16_t* wn;    // bf16 [N]
-    float* Y;              // [M][ldy]
+    void* Y;               // fp32 or bf16 [M][ldy]
     int64_t M, N, ldy;
     int K;
-    int vec4;              // Y and ldy allow 16-byte row stores; wn allows 8-byte loads
+    int vec4;              // Y, ldy, wn and bias allow 4-wide row stores and loads
+    const uint16_t* bias;  // bf16 [N] or null, added after the rescaling
+    int gelu;              // apply x * Phi(x) (exact erf) after the bias
+    int out_bf16;          // store Y as bf16 (round to nearest even) instead of fp32
     uint16_t lut_a[16];    // fp16 levels (2^ba used)
     uint16_t lut_w[16];    // fp16 levels (2^bw used)
 };

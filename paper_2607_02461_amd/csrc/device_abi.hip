@@ -197,9 +197,10 @@ orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t
     return quantize_rows("rpbh_quantize_act", p, cb_a, X, M, K, ldx, eps, x_codes, x_norm, false, stream);
 }
 
-orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
-                           orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N, int64_t K,
-                           float* Y, int64_t ldy, void* stream) {
+orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                              orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
+                              int64_t K, const uint16_t* bias, int32_t act, int32_t out_dtype, void* Y, int64_t ldy,
+                              void* stream) {
     clear_error();
     if (!cb_a || !cb_w) return fail(ORBIT_EINVAL, "orbit_qlinear: codebook is NULL");
     if (M < 0 || N < 0) return fail(ORBIT_EINVAL, "orbit_qlinear: negative M or N");
@@ -207,12 +208,17 @@ orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const fl
         return fail(ORBIT_EINVAL, "orbit_qlinear: K=%lld but codebooks have d=%lld and d=%lld", (long long)K,
                     (long long)cb_a->d, (long long)cb_w->d);
     if (ldy < N) return fail(ORBIT_EINVAL, "orbit_qlinear: ldy=%lld < N=%lld", (long long)ldy, (long long)N);
+    if (act != ORBIT_ACT_NONE && act != ORBIT_ACT_GELU) return fail(ORBIT_EINVAL, "orbit_qlinear: unknown act %d", act);
+    if (out_dtype != ORBIT_OUT_F32 && out_dtype != ORBIT_OUT_BF16)
+        return fail(ORBIT_EINVAL, "orbit_qlinear: unknown out_dtype %d", out_dtype);
     if (cb_a->bits < 2 || cb_a->bits > 4 || cb_w->bits < 2 || cb_w->bits > 4)
         return fail(ORBIT_EUNSUPPORTED, "orbit_qlinear: bit-widths (%d, %d) not implemented (2..4 are)", cb_a->bits, cb_w->bits);
     if (K % 64 != 0 || K > (int64_t)1 << 30) return fail(ORBIT_EUNSUPPORTED, "orbit_qlinear: K=%lld must be a multiple of 64", (long long)K);
     if (M == 0 || N == 0) return ORBIT_OK;
+    const int ysize = out_dtype == ORBIT_OUT_BF16 ? 2 : 4;
     if (!x_codes || !x_norm || !w_codes || !w_norm || !Y) return fail(ORBIT_EINVAL, "orbit_qlinear: null device pointer");
-    if (!aligned(x_codes, 16) || !aligned(w_codes, 16) || !aligned(x_norm, 4) || !aligned(w_norm, 2) || !aligned(Y, 4))
+    if (!aligned(x_codes, 16) || !aligned(w_codes, 16) || !aligned(x_norm, 4) || !aligned(w_norm, 2) ||
+        !aligned(Y, ysize) || (bias && !aligned(bias, 2)))
         return fail(ORBIT_EINVAL, "orbit_qlinear: misaligned pointer (codes need 16 bytes)");
     int dev;
     DeviceInfo info;
@@ -228,7 +234,10 @@ orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const fl
     g.N = N;
     g.ldy = ldy;
     g.K = (int)K;
-    g.vec4 = aligned(Y, 16) && ldy % 4 == 0 && aligned(w_norm, 8);
+    g.bias = bias;
+    g.gelu = act == ORBIT_ACT_GELU;
+    g.out_bf16 = out_dtype == ORBIT_OUT_BF16;
+    g.vec4 = aligned(Y, 4 * ysize) && ldy % 4 == 0 && aligned(w_norm, 8) && (!bias || aligned(bias, 8));
     for (const orbit_codebook_s* cb : {cb_a, cb_w}) {
         // the 4-bit decoder reads the positive half and mirrors it
         if (cb->bits != 4) continue;
@@ -243,6 +252,13 @@ orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const fl
     hipError_t e = launch_lut_gemm(g, cb_a->bits, cb_w->bits, info.cus, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "orbit_qlinear");
     return ORBIT_OK;
+}
+
+orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                           orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N, int64_t K,
+                           float* Y, int64_t ldy, void* stream) {
+    return orbit_qlinear_ex(cb_a, x_codes, x_norm, M, cb_w, w_codes, w_norm, N, K, nullptr, ORBIT_ACT_NONE,
+                            ORBIT_OUT_F32, Y, ldy, stream);
 }
 
 }  // extern "C"

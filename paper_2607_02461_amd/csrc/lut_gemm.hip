@@ -130,6 +130,26 @@ __device__ __forceinline__ void load_codes32(const uint8_t* src, uint32_t (&w)[4
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t v) { return __uint_as_float((uint32_t)v << 16); }
 
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
+    const uint32_t u = __float_as_uint(x);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;  // NaN stays NaN
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// The rest of the layer after the rescaled contraction: bias, then GELU (x * Phi(x), exact erf).
+__device__ __forceinline__ float epilogue_value(const GemmParams& p, float v, float bias) {
+    v += bias;
+    if (p.gelu) v = 0.5f * v * (1.f + erff(v * 0.7071067811865476f));
+    return v;
+}
+
+__device__ __forceinline__ void store_one(const GemmParams& p, int64_t row, int64_t col, float v) {
+    if (p.out_bf16)
+        ((uint16_t*)p.Y)[row * p.ldy + col] = (uint16_t)f32_to_bf16_rne(v);
+    else
+        ((float*)p.Y)[row * p.ldy + col] = v;
+}
+
 template <int BA, int BW>
 __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     __shared__ __align__(16) _Float16 As[BM * LDS_STRIDE];
@@ -196,10 +216,11 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
             const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
             if (col >= p.N) continue;
             const float rw = bf16_to_f32(p.wn[col]);
+            const float bias = p.bias ? bf16_to_f32(p.bias[col]) : 0.f;
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const int64_t row = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                if (row < p.M) p.Y[row * p.ldy + col] = acc[i][j][e] * p.xn[row] * rw;
+                if (row < p.M) store_one(p, row, col, epilogue_value(p, acc[i][j][e] * p.xn[row] * rw, bias));
             }
         }
     }
@@ -345,7 +366,8 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
 
     // epilogue.  The MFMAs computed the transposed tile, so element e of accumulator (i, j)
     // belongs to row i*32 + lane%32 and column j*32 + 8*(e/4) + 4*(lane/32) + e%4: each lane
-    // holds runs of four consecutive columns of one row and stores them as one 16-byte vector.
+    // holds runs of four consecutive columns of one row and stores them as one vector (16 bytes
+    // of fp32 or 8 of bf16).
     const int64_t col0 = n0 + wn * 64 + 4 * (lane >> 5);
     uint2 rwv[2][4];  // bf16 r' of the lane's columns, four per (j, run)
 #pragma unroll
@@ -362,30 +384,42 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
                 rwv[j][q] = make_uint2(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16));
             }
         }
+    const bool plain = !p.bias && !p.gelu && !p.out_bf16;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int64_t row = m0 + wm * 128 + i * 32 + (lane & 31);
         if (row >= p.M) continue;
         const float xs = p.xn[row];
-        float* yrow = p.Y + row * p.ldy;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int64_t c = col0 + j * 32 + 8 * q;
                 const uint2 rw = rwv[j][q];
-                float4 v;
-                v.x = acc[i][j][4 * q + 0] * xs * __uint_as_float(rw.x << 16);
-                v.y = acc[i][j][4 * q + 1] * xs * __uint_as_float(rw.x & 0xFFFF0000u);
-                v.z = acc[i][j][4 * q + 2] * xs * __uint_as_float(rw.y << 16);
-                v.w = acc[i][j][4 * q + 3] * xs * __uint_as_float(rw.y & 0xFFFF0000u);
-                if (c + 3 < p.N && p.vec4) {
-                    *(float4*)(yrow + c) = v;
+                float v[4] = {acc[i][j][4 * q + 0] * xs * __uint_as_float(rw.x << 16),
+                              acc[i][j][4 * q + 1] * xs * __uint_as_float(rw.x & 0xFFFF0000u),
+                              acc[i][j][4 * q + 2] * xs * __uint_as_float(rw.y << 16),
+                              acc[i][j][4 * q + 3] * xs * __uint_as_float(rw.y & 0xFFFF0000u)};
+                const bool full = c + 3 < p.N && p.vec4;
+                if (plain && full) {
+                    *(float4*)((float*)p.Y + row * p.ldy + c) = make_float4(v[0], v[1], v[2], v[3]);
+                    continue;
+                }
+                if (!plain) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        v[r] = epilogue_value(p, v[r], p.bias && c + r < p.N ? bf16_to_f32(p.bias[c + r]) : 0.f);
+                }
+                if (full && p.out_bf16) {
+                    *(uint2*)((uint16_t*)p.Y + row * p.ldy + c) =
+                        make_uint2(f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16),
+                                   f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16));
+                } else if (full) {
+                    *(float4*)((float*)p.Y + row * p.ldy + c) = make_float4(v[0], v[1], v[2], v[3]);
                 } else {
-                    if (c + 0 < p.N) yrow[c + 0] = v.x;
-                    if (c + 1 < p.N) yrow[c + 1] = v.y;
-                    if (c + 2 < p.N) yrow[c + 2] = v.z;
-                    if (c + 3 < p.N) yrow[c + 3] = v.w;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (c + r < p.N) store_one(p, row, c + r, v[r]);
                 }
             }
         }

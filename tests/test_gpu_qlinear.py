@@ -61,6 +61,51 @@ def test_random_codes_large_tiles(M, N, K, ba, bw):
     assert worst_row <= GEMM_REL_F
 
 
+# the fused layer epilogue (bias, GELU, bf16 output) on both kernels, with vector and element-wise
+# stores (ldy a multiple of 4 or not)
+@pytest.mark.parametrize("M,N,K", [(300, 130, 512), (4133, 8061, 192)])
+@pytest.mark.parametrize("bias,gelu,bf16", [(True, False, False), (False, True, False), (False, False, True),
+                                            (True, True, True)])
+@pytest.mark.parametrize("pad", [0, 1])
+def test_fused_epilogue(M, N, K, bias, gelu, bf16, pad):
+    ba, bw = 4, 4 if M < 1000 else 3
+    xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K + 7)
+    cba, cbw = oq.lloydmax_codebook(ba, K), oq.lloydmax_codebook(bw, K)
+    xp = torch.from_numpy(oracle.pack_codes(xc.numpy(), ba)).to(DEV)
+    wp = torch.from_numpy(oracle.pack_codes(wc.numpy(), bw)).to(DEV)
+    g = torch.Generator()
+    g.manual_seed(N)
+    b = torch.randn(N, generator=g).to(torch.bfloat16) if bias else None
+    dt = torch.bfloat16 if bf16 else torch.float32
+    out = torch.full((M, N + pad), float("nan"), dtype=dt, device=DEV)[:, :N]
+    Y = oq.orbit_qlinear_ex(cba, xp, xs.to(DEV), cbw, wp, wr.to(DEV), bias=b.to(DEV) if bias else None,
+                            gelu=gelu, out_dtype=dt, out=out)
+    torch.cuda.synchronize()
+    Yn = Y.float().cpu().numpy().astype(np.float64)
+    base = qlinear_oracle_fp16(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
+    ref = oracle.layer_epilogue(base, bias=b.double().numpy() if bias else None, gelu=gelu)
+    err = rel_frobenius(Yn, ref)
+    stats = {"rel_f": err}
+    if bf16:
+        # every bf16 output is the rounding of a value within the fp32 accumulation error of the
+        # fp64 result: at most one bf16 ulp from it, plus an absolute slack of 1e-5 of the
+        # largest output for values that cancel to almost nothing; mostly exactly the rounding
+        rb = oracle.layer_epilogue(base, bias=b.double().numpy() if bias else None, gelu=gelu, out_bf16=True)
+        ulp = np.ldexp(1.0, np.frexp(np.maximum(np.abs(ref), 1e-30))[1] - 8)
+        far = np.abs(Yn - ref) > ulp + 1e-5 * np.max(np.abs(ref))
+        stats.update(equal_to_rounding=float(np.mean(Yn == rb)), beyond=int(far.sum()),
+                     rel_f_vs_rounded=rel_frobenius(Yn, rb))
+        assert not far.any()
+        assert np.mean(Yn == rb) > 0.999
+        # bf16 output alone carries ~1.7e-3 of rounding (8 significant bits); the bar applies to
+        # the kernel's difference from the correctly rounded layer
+        err = rel_frobenius(Yn, rb)
+    log_stats(f"fused epilogue M={M} N={N} K={K} bias={bias} gelu={gelu} bf16={bf16} pad={pad}", **stats)
+    assert err <= GEMM_REL_F
+    if pad:
+        assert torch.isnan(out.float()).sum() == 0      # every valid element written
+
+
 def test_constant_codes_closed_form():
     M, N, K = 70, 200, 1024
     cba, cbw = oq.lloydmax_codebook(4, K), oq.lloydmax_codebook(3, K)

@@ -168,3 +168,19 @@ def test_near_tie_mask_matches_bruteforce_distance():
                         cb.thresholds + 3e-6, cb.thresholds - 2e-5])
     brute = np.min(np.abs(u[:, None] - cb.thresholds[None, :]), axis=1) <= 1e-5
     assert np.array_equal(oracle.near_tie_mask(u, cb.thresholds, 1e-5), brute)
+
+
+def test_layer_epilogue_closed_forms():
+    # GELU(x) = x * Phi(x): Phi(1) = 0.841344746068543, Phi(-1) = 1 - Phi(1), GELU(0) = 0, and
+    # GELU(x) - GELU(-x) = x for every x
+    Y = np.array([[0.0, 1.0, -1.0, 3.0, -3.0]])
+    g = oracle.layer_epilogue(Y, gelu=True)
+    assert g[0, 0] == 0.0
+    assert abs(g[0, 1] - 0.8413447460685429) < 1e-15
+    assert abs(g[0, 2] + 0.15865525393145707) < 1e-15
+    assert np.allclose(g[0, 1::2] - g[0, 2::2], Y[0, 1::2], atol=1e-15)
+    # bias is added before the activation; bf16 output is the RNE rounding of the fp64 value
+    b = np.array([0.5, 0.0, 0.0, 0.0, 0.0])
+    assert abs(oracle.layer_epilogue(Y, bias=b, gelu=True)[0, 0] - 0.5 * 0.6914624612740131) < 1e-15
+    r = oracle.layer_epilogue(np.array([[1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -9]]), out_bf16=True)
+    assert r[0, 0] == 1.0 and r[0, 1] == 1.0 + 2 ** -6 and r[0, 2] == 1.0   # half-ulp ties go to even
