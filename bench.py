@@ -290,6 +290,33 @@ def main():
              "tflops": float(flops[0]) / (fused_ms * 1e-3) / 1e12, "plain_fp32_ms": float(gemm_ms[0])}
     del Yb
 
+    # NEXT row: the video recipe's 6-bit activations (W4A6, the paper's Wan setting) on the
+    # up-projection: the quantizer writing 6-bit codes and the GEMM decoding them
+    cb6 = oq.lloydmax_codebook(6, K0)
+    xc6 = torch.empty((L0["lin"].M, K0 * 6 // 8), dtype=torch.uint8, device=dev)
+    plan0 = L0["plan"]
+    for _ in range(2):
+        oq.rpbh_quantize_act(plan0, cb6, L0["X"], 1e-10, xc6, L0["xn"])
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        oq.rpbh_quantize_act(plan0, cb6, L0["X"], 1e-10, xc6, L0["xn"])
+    e1.record()
+    torch.cuda.synchronize()
+    q6_ms = e0.elapsed_time(e1) / 10
+    for _ in range(2):
+        oq.orbit_qlinear(cb6, xc6, L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"])
+    e0.record()
+    for _ in range(5):
+        oq.orbit_qlinear(cb6, xc6, L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"])
+    e1.record()
+    torch.cuda.synchronize()
+    g6_ms = e0.elapsed_time(e1) / 5
+    q6_bytes = quant_bytes(L0["lin"].M, K0, 6)
+    a6 = {"linear": L0["lin"].name, "quant_ms": q6_ms, "quant_gbs": q6_bytes / (q6_ms * 1e-3) / 1e9,
+          "gemm_ms": g6_ms, "gemm_tflops": float(flops[0]) / (g6_ms * 1e-3) / 1e12}
+    del xc6
+
     cpu = None
     if args.cpu_baseline_rows > 0:
         cpu = cpu_baseline(layers, args.cpu_baseline_rows)
@@ -332,6 +359,7 @@ def main():
         "quantizer_paper_block_rule": paper_h,
         "rotation_classes": rot,
         "fused_epilogue": fused,
+        "w4a6": a6,
         "cpu_baseline": cpu,
         "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0)},
     }

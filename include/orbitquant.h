@@ -98,7 +98,8 @@ void rpbh_plan_destroy(orbit_plan p);
  * f_d(t) = Gamma(d/2) / (sqrt(pi) Gamma((d-1)/2)) (1 - t^2)^((d-3)/2) on [-1, 1]
  * (Sec. 3.2, Eqs. (2)-(3); Sec. 4.5; Alg. 1, offline stage).  Host only.
  *
- *   bits  1..6 for the codebook itself; the kernels accept 2, 3 and 4
+ *   bits  1..6 for the codebook itself; the quantizer accepts 2, 3, 4 and 6, the GEMM 2, 3, 4
+ *         and 6 for activations and 2..4 for weights
  *   d     input dimension, >= 3
  *
  * Computed in fp64 by the fixed-point iteration of the midpoint and centroid conditions on
@@ -130,7 +131,7 @@ void lloydmax_codebook_destroy(orbit_codebook c);
  * fp32 norm; only the stored magnitude is rounded.
  *
  *   p       plan with plan.d == K
- *   cb_w    codebook with cb.d == K and cb.bits = b_w in {2, 3, 4}
+ *   cb_w    codebook with cb.d == K and cb.bits = b_w in {2, 3, 4, 6} (the GEMM takes 2..4)
  *   W       device, bf16 [N][ldw]; row i is w_i (the layout of nn.Linear.weight)
  *   N, K    rows and input dimension; N >= 0
  *   ldw     row stride of W in elements, >= K and a multiple of 8
@@ -144,7 +145,8 @@ void lloydmax_codebook_destroy(orbit_codebook c);
  *
  * Pointers: W and w_codes 16-byte aligned, w_norm 2-byte aligned.
  * Errors: ORBIT_EINVAL (null pointer, K mismatch, ldw, alignment); ORBIT_EUNSUPPORTED
- * (h outside 128..4096, K > 16384 or bits outside 2..4); ORBIT_EHIP.  N = 0 returns at once.
+ * (h outside 128..4096, K > 16384 or bits not in {2, 3, 4, 6}); ORBIT_EHIP.  N = 0 returns at
+ * once.  Packing as above: at b = 6 every 4 codes fill 3 bytes.
  */
 orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const uint16_t* W, int64_t N,
                                       int64_t K, int64_t ldw, float eps, uint8_t* w_codes,
@@ -187,7 +189,8 @@ orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t
  * handled element-wise).  The 4-bit decoder relies on the codebook's exact antisymmetry in
  * fp16 (L[15-c] = -L[c]), which lloydmax_codebook guarantees; ORBIT_EINTERNAL otherwise.
  * Errors: ORBIT_EINVAL (null pointer, dimension mismatch, ldy < N); ORBIT_EUNSUPPORTED
- * (bits outside 2..4, K not a multiple of 64); ORBIT_EHIP.  M = 0 or N = 0 returns at once.
+ * (activation bits not in {2, 3, 4, 6}, weight bits outside 2..4, K not a multiple of 64);
+ * ORBIT_EHIP.  M = 0 or N = 0 returns at once.
  */
 orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
                            orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,

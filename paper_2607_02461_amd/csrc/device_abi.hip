@@ -15,7 +15,7 @@ namespace {
 constexpr int kQuantH = 128;       // the fused quantizer's in-register transform (larger h adds stages)
 constexpr int64_t kQuantMaxK = 16384;
 constexpr int kQuantMaxH = 4096;  // block sizes 128 .. 4096 (the FWHT's stages across blocks)
-constexpr int kQuantMaxCells = 2048;  // encoder table cells (LDS budget)
+constexpr int kQuantMaxCells = 8192;  // encoder table cells (LDS budget; 6-bit tables reach ~4300 at K = 16384)
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
@@ -107,7 +107,8 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     if (p->h < kQuantH || p->h > kQuantMaxH)
         return fail(ORBIT_EUNSUPPORTED, "%s: block size h=%d not implemented (powers of two 128..%d are)", who, p->h,
                     kQuantMaxH);
-    if (cb->bits < 2 || cb->bits > 4) return fail(ORBIT_EUNSUPPORTED, "%s: %d-bit codes not implemented (2..4 are)", who, cb->bits);
+    if (cb->bits < 2 || cb->bits > 6 || cb->bits == 5)
+        return fail(ORBIT_EUNSUPPORTED, "%s: %d-bit codes not implemented (2, 3, 4 and 6 are)", who, cb->bits);
     if (K > kQuantMaxK) return fail(ORBIT_EUNSUPPORTED, "%s: K=%lld above %lld", who, (long long)K, (long long)kQuantMaxK);
     if ((int64_t)quant_rows_per_group((int)K) * ldx * 2 >= ((int64_t)1 << 31))
         return fail(ORBIT_EUNSUPPORTED, "%s: row stride %lld too large", who, (long long)ldx);
@@ -211,8 +212,10 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
     if (act != ORBIT_ACT_NONE && act != ORBIT_ACT_GELU) return fail(ORBIT_EINVAL, "orbit_qlinear: unknown act %d", act);
     if (out_dtype != ORBIT_OUT_F32 && out_dtype != ORBIT_OUT_BF16)
         return fail(ORBIT_EINVAL, "orbit_qlinear: unknown out_dtype %d", out_dtype);
-    if (cb_a->bits < 2 || cb_a->bits > 4 || cb_w->bits < 2 || cb_w->bits > 4)
-        return fail(ORBIT_EUNSUPPORTED, "orbit_qlinear: bit-widths (%d, %d) not implemented (2..4 are)", cb_a->bits, cb_w->bits);
+    if (cb_a->bits < 2 || cb_a->bits > 6 || cb_a->bits == 5 || cb_w->bits < 2 || cb_w->bits > 4)
+        return fail(ORBIT_EUNSUPPORTED,
+                    "orbit_qlinear: bit-widths (a %d, w %d) not implemented (activations 2, 3, 4, 6; weights 2..4)",
+                    cb_a->bits, cb_w->bits);
     if (K % 64 != 0 || K > (int64_t)1 << 30) return fail(ORBIT_EUNSUPPORTED, "orbit_qlinear: K=%lld must be a multiple of 64", (long long)K);
     if (M == 0 || N == 0) return ORBIT_OK;
     const int ysize = out_dtype == ORBIT_OUT_BF16 ? 2 : 4;
@@ -245,10 +248,8 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
             if (cb->lut_f16[15 - c] != (uint16_t)(cb->lut_f16[c] ^ 0x8000u))
                 return fail(ORBIT_EINTERNAL, "orbit_qlinear: 4-bit fp16 levels are not antisymmetric");
     }
-    for (int j = 0; j < 16; ++j) {
-        g.lut_a[j] = j < (1 << cb_a->bits) ? cb_a->lut_f16[j] : 0;
-        g.lut_w[j] = j < (1 << cb_w->bits) ? cb_w->lut_f16[j] : 0;
-    }
+    for (int j = 0; j < 64; ++j) g.lut_a[j] = j < (1 << cb_a->bits) ? cb_a->lut_f16[j] : 0;
+    for (int j = 0; j < 16; ++j) g.lut_w[j] = j < (1 << cb_w->bits) ? cb_w->lut_f16[j] : 0;
     hipError_t e = launch_lut_gemm(g, cb_a->bits, cb_w->bits, info.cus, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "orbit_qlinear");
     return ORBIT_OK;

@@ -24,6 +24,10 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int BM = 128, BN = 128, BK = 64;
 constexpr int LDS_STRIDE = BK + 8;  // halves per tile row (padding against bank conflicts)
 
+// 32 packed codes of one row: 4*BITS bytes, in BITS words (4 words for 2- and 3-bit codes too)
+template <int BITS>
+using Codes = uint32_t[BITS == 6 ? 6 : 4];
+
 struct ByteTables {
     uint32_t lo[2], hi[2];  // byte e of lo[e/4] (hi[e/4]) is the low (high) byte of table entry e
 };
@@ -34,7 +38,7 @@ struct ByteTables {
 // antisymmetry bit for bit before launching.
 template <int BITS>
 __device__ __forceinline__ ByteTables make_tables(const uint16_t* lut) {
-    constexpr int n = BITS == 4 ? 8 : 1 << BITS, first = BITS == 4 ? 8 : 0;
+    constexpr int n = BITS == 4 ? 8 : BITS == 6 ? 0 : 1 << BITS, first = BITS == 4 ? 8 : 0;
     ByteTables t;
 #pragma unroll
     for (int w = 0; w < 2; ++w) {
@@ -71,7 +75,7 @@ __device__ __forceinline__ void interleave(uint32_t lo, uint32_t hi, uint32_t& d
 
 // 2- and 3-bit groups: every level is in the table
 template <int BITS>
-__device__ __forceinline__ void decode8_small(const uint32_t (&w)[4], int g, const ByteTables& t, uint32_t (&out)[4]) {
+__device__ __forceinline__ void decode8_small(const Codes<BITS>& w, int g, const ByteTables& t, uint32_t (&out)[4]) {
     uint32_t lo, hi;
     uint32_t ce, co;  // codes k0 k2 k4 k6 and k1 k3 k5 k7, one per byte
     if constexpr (BITS == 2) {
@@ -93,12 +97,33 @@ __device__ __forceinline__ void decode8_small(const uint32_t (&w)[4], int g, con
     interleave(lo, hi, out[2], out[3]);
 }
 
+// 6-bit groups: 64 levels are too many for byte permutes, so the fp16 levels sit in a 64-entry
+// LDS table with a 4-byte stride; every entry has its own bank, so a wave's 64 lookups never
+// conflict (equal codes broadcast).
+__device__ __forceinline__ void decode8_lds6(const Codes<6>& w, int g, const uint32_t* tab, uint32_t (&out)[4]) {
+    // group g covers bits 48g .. 48g+47 of the 192-bit stream (selects, not an indexed load from
+    // the register array)
+    const uint32_t lo = g == 0 ? w[0] : g == 1 ? w[1] : g == 2 ? w[3] : w[4];
+    const uint32_t hi = g == 0 ? w[1] : g == 1 ? w[2] : g == 2 ? w[4] : w[5];
+    const uint64_t x = (((uint64_t)hi << 32) | lo) >> ((g & 1) * 16);
+    uint32_t v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = tab[(uint32_t)(x >> (6 * j)) & 63u];
+    out[0] = v[0] | (v[2] << 16);
+    out[1] = v[4] | (v[6] << 16);
+    out[2] = v[1] | (v[3] << 16);
+    out[3] = v[5] | (v[7] << 16);
+}
+
 // Group g (codes 8g .. 8g+7) of 32 packed codes (4*BITS bytes, LSB-first) -> four fp16x2 words
 // in canonical slot order.
 template <int BITS>
-__device__ __forceinline__ void decode8(const uint32_t (&w)[4], int g, const ByteTables& t, uint32_t (&out)[4]) {
+__device__ __forceinline__ void decode8(const Codes<BITS>& w, int g, const ByteTables& t, const uint32_t* tab6,
+                                        uint32_t (&out)[4]) {
     uint32_t lo, hi;
-    if constexpr (BITS == 4) {
+    if constexpr (BITS == 6) {
+        decode8_lds6(w, g, tab6, out);
+    } else if constexpr (BITS == 4) {
         // nibble j of x is code k_j; neg has bit 3 of each nibble set where that code is below 8
         // (a negative level); there the low three bits are mirrored (j -> 7 - j) to index the
         // positive half, and the sign bit is set on the high byte afterwards
@@ -115,10 +140,14 @@ __device__ __forceinline__ void decode8(const uint32_t (&w)[4], int g, const Byt
 }
 
 template <int BITS>
-__device__ __forceinline__ void load_codes32(const uint8_t* src, uint32_t (&w)[4]) {
+__device__ __forceinline__ void load_codes32(const uint8_t* src, Codes<BITS>& w) {
     if constexpr (BITS == 4) {
         const uint4 v = *(const uint4*)src;
         w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+    } else if constexpr (BITS == 6) {
+        // 24 bytes at an 8-byte aligned offset
+        const uint2 a = *(const uint2*)src, b = *(const uint2*)(src + 8), c = *(const uint2*)(src + 16);
+        w[0] = a.x; w[1] = a.y; w[2] = b.x; w[3] = b.y; w[4] = c.x; w[5] = c.y;
     } else if constexpr (BITS == 2) {
         const uint2 v = *(const uint2*)src;
         w[0] = v.x; w[1] = v.y; w[2] = 0; w[3] = 0;
@@ -154,11 +183,16 @@ template <int BA, int BW>
 __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     __shared__ __align__(16) _Float16 As[BM * LDS_STRIDE];
     __shared__ __align__(16) _Float16 Bs[BN * LDS_STRIDE];
+    __shared__ uint32_t tab6[BA == 6 ? 64 : 1];  // 6-bit activation levels (fp16 in the low half)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
     const ByteTables ta = make_tables<BA>(p.lut_a);
     const ByteTables tw = make_tables<BW>(p.lut_w);
+    if constexpr (BA == 6) {
+        if (tid < 64) tab6[tid] = p.lut_a[tid];
+        __syncthreads();
+    }
 
     // this thread decodes 32 codes of one A row and 32 codes of one B row per K-step
     const int lr = tid >> 1, lh = tid & 1;
@@ -176,7 +210,8 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
     for (int k0 = 0; k0 < p.K; k0 += BK) {
-        uint32_t wa[4], wb[4];
+        Codes<BA> wa;
+        Codes<BW> wb;
         load_codes32<BA>(asrc + (int64_t)k0 * BA / 8, wa);
         load_codes32<BW>(bsrc + (int64_t)k0 * BW / 8, wb);
         uint4* adst = (uint4*)(As + lr * LDS_STRIDE + lh * 32);
@@ -184,8 +219,8 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             uint32_t da[4], db[4];
-            decode8<BA>(wa, g, ta, da);
-            decode8<BW>(wb, g, tw, db);
+            decode8<BA>(wa, g, ta, tab6, da);
+            decode8<BW>(wb, g, tw, nullptr, db);
             adst[g] = make_uint4(da[0], da[1], da[2], da[3]);
             bdst[g] = make_uint4(db[0], db[1], db[2], db[3]);
         }
@@ -259,6 +294,11 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
 
     const ByteTables ta = make_tables<BA>(p.lut_a);
     const ByteTables tw = make_tables<BW>(p.lut_w);
+    uint32_t* const tab6 = (uint32_t*)(lds + 2 * 2 * LDS2_TILE);  // 6-bit levels, after the tiles
+    if constexpr (BA == 6) {
+        if (tid < 64) tab6[tid] = p.lut_a[tid];
+        __syncthreads();
+    }
 
     // this thread decodes 32 codes of one A row and 32 codes of one B row per K-step
     const int lr = tid >> 1, lh = tid & 1;
@@ -281,14 +321,15 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     const _Float16* const b_frag0 = lds + LDS2_TILE + (wn * 64 + (lane & 31)) * LDS2_STRIDE + (lane >> 5) * 8;
     constexpr int STAGE = 2 * LDS2_TILE;
 
-    uint32_t wa[4], wb[4];
+    Codes<BA> wa, xa;
+    Codes<BW> wb, xb;
     load_codes32<BA>(asrc, wa);
     load_codes32<BW>(bsrc, wb);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
         uint32_t da[4], db[4];
-        decode8<BA>(wa, g, ta, da);
-        decode8<BW>(wb, g, tw, db);
+        decode8<BA>(wa, g, ta, tab6, da);
+        decode8<BW>(wb, g, tw, nullptr, db);
         *(uint4*)(a_dst0 + 8 * g) = make_uint4(da[0], da[1], da[2], da[3]);
         *(uint4*)(a_dst0 + LDS2_TILE + 8 * g) = make_uint4(db[0], db[1], db[2], db[3]);
     }
@@ -303,8 +344,7 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     // the other stage and the codes of step s+2 load into (na, nb).  The loop below is unrolled
     // by two so that the code registers swap roles instead of being copied (a copy would wait
     // for the load).
-    auto kstep = [&](int s, const uint32_t (&ca)[4], const uint32_t (&cb)[4], uint32_t (&na)[4],
-                     uint32_t (&nb)[4]) {
+    auto kstep = [&](int s, const Codes<BA>& ca, const Codes<BW>& cb, Codes<BA>& na, Codes<BW>& nb) {
         // the last steps re-load the final step's codes; they are never used
         const int64_t s2 = min(s + 2, nk - 1);
         load_codes32<BA>(asrc + s2 * astep, na);
@@ -332,8 +372,8 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
             // before the previous barrier); on the final step this refills a stage nobody reads
             {
                 uint32_t da[4], db[4];
-                decode8<BA>(ca, kk, ta, da);
-                decode8<BW>(cb, kk, tw, db);
+                decode8<BA>(ca, kk, ta, tab6, da);
+                decode8<BW>(cb, kk, tw, nullptr, db);
                 *(uint4*)(a_dst0 + nxt + 8 * kk) = make_uint4(da[0], da[1], da[2], da[3]);
                 *(uint4*)(a_dst0 + nxt + LDS2_TILE + 8 * kk) = make_uint4(db[0], db[1], db[2], db[3]);
             }
@@ -356,7 +396,6 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
         __syncthreads();
     };
 
-    uint32_t xa[4], xb[4];
     int s = 0;
     for (; s + 1 < nk; s += 2) {
         kstep(s, wa, wb, xa, xb);
@@ -429,7 +468,7 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
 template <int BA, int BW>
 hipError_t launch_big(const GemmParams& p, hipStream_t stream) {
     static bool attr = false;
-    const size_t smem = (size_t)2 * 2 * LDS2_TILE * sizeof(_Float16);
+    const size_t smem = (size_t)2 * 2 * LDS2_TILE * sizeof(_Float16) + (BA == 6 ? 64 * sizeof(uint32_t) : 0);
     if (!attr) {
         hipError_t e = hipFuncSetAttribute((const void*)lut_gemm_big<BA, BW>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)smem);
@@ -462,6 +501,9 @@ hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, int cus, hipStre
         case 3 * 8 + 2: return launch_one<3, 2>(p, stream, cus);
         case 3 * 8 + 3: return launch_one<3, 3>(p, stream, cus);
         case 3 * 8 + 4: return launch_one<3, 4>(p, stream, cus);
+        case 6 * 8 + 2: return launch_one<6, 2>(p, stream, cus);
+        case 6 * 8 + 3: return launch_one<6, 3>(p, stream, cus);
+        case 6 * 8 + 4: return launch_one<6, 4>(p, stream, cus);
         case 4 * 8 + 2: return launch_one<4, 2>(p, stream, cus);
         case 4 * 8 + 3: return launch_one<4, 3>(p, stream, cus);
         default: return launch_one<4, 4>(p, stream, cus);

@@ -137,9 +137,14 @@ __device__ __forceinline__ void stage1(uint32_t P, uint32_t one_one, float& sum,
 }
 
 template <int BITS>
-__device__ __forceinline__ void store_packed(uint8_t* dst, const uint32_t (&w)[4]) {
+__device__ __forceinline__ void store_packed(uint8_t* dst, const uint32_t (&w)[6]) {
     if constexpr (BITS == 4) {
         *(uint4*)dst = make_uint4(w[0], w[1], w[2], w[3]);
+    } else if constexpr (BITS == 6) {
+        // 24 bytes at an 8-byte aligned offset
+        *(uint2*)dst = make_uint2(w[0], w[1]);
+        *(uint2*)(dst + 8) = make_uint2(w[2], w[3]);
+        *(uint2*)(dst + 16) = make_uint2(w[4], w[5]);
     } else if constexpr (BITS == 2) {
         *(uint2*)dst = make_uint2(w[0], w[1]);
     } else {
@@ -160,8 +165,28 @@ __device__ __forceinline__ uint32_t code_byte(float y, uint32_t into) {
 // bytes.  v_cvt_pk_u8_f32 converts a value and inserts it as one byte of a word in a single op;
 // the codes are spread over bytes so that a few shifts and ORs close the gaps between them.
 template <int BITS>
-__device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[4]) {
-    if constexpr (BITS == 4) {
+__device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[6]) {
+    if constexpr (BITS == 6) {
+        // 4 codes = 24 bits: the bytes of A are codes 4i .. 4i+3, then the gaps close; eight
+        // 24-bit groups fill six words
+        uint32_t g[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float* v = y + 4 * i;
+            uint32_t A = code_byte<0>(v[0], 0u);
+            A = code_byte<1>(v[1], A);
+            A = code_byte<2>(v[2], A);
+            A = code_byte<3>(v[3], A);
+            g[i] = (A & 0x3Fu) | ((A >> 2) & 0xFC0u) | ((A >> 4) & 0x3F000u) | ((A >> 6) & 0xFC0000u);
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            w[3 * h + 0] = g[4 * h] | (g[4 * h + 1] << 24);
+            w[3 * h + 1] = (g[4 * h + 1] >> 8) | (g[4 * h + 2] << 16);
+            w[3 * h + 2] = (g[4 * h + 2] >> 16) | (g[4 * h + 3] << 8);
+        }
+        return;
+    } else if constexpr (BITS == 4) {
         // bytes of A = codes 8i, 8i+2, 8i+4, 8i+6 and of B = codes 8i+1, 8i+3, ...: A | B << 4
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -191,7 +216,7 @@ __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[4
             }
             w[i] = D[0] | (D[1] << 2) | (D[2] << 4) | (D[3] << 6);
         }
-        w[2] = w[3] = 0u;
+        w[2] = w[3] = w[4] = w[5] = 0u;
     } else {
         static_assert(BITS == 3, "bits");
         // 8 codes = 24 bits: codes 2j, 2j+1 share byte j of P (6 bits), then the gaps close
@@ -212,7 +237,7 @@ __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[4
         w[0] = g[0] | (g[1] << 24);
         w[1] = (g[1] >> 8) | (g[2] << 16);
         w[2] = (g[2] >> 16) | (g[3] << 8);
-        w[3] = 0u;
+        w[3] = w[4] = w[5] = 0u;
     }
 }
 
@@ -377,7 +402,7 @@ struct Quantizer {
             const float t = fmaf(z[r], a, c);
             y[r] = fmaf(t, 0.5f, tab[(uint32_t)t]);
         }
-        uint32_t w[4];
+        uint32_t w[6];
         pack_codes<BITS>(y, w);
         if (owner)
             store_packed<BITS>(p.codes + (row0 + rg) * ((int64_t)p.K * BITS / 8) + (int64_t)(blk * 4 + q) * 4 * BITS, w);
@@ -473,6 +498,7 @@ hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, 
     do {                                                                                           \
         if (bits == 2) ORBIT_LAUNCH(2, NB, OU);                                                    \
         else if (bits == 3) ORBIT_LAUNCH(3, NB, OU);                                               \
+        else if (bits == 6) ORBIT_LAUNCH(6, NB, OU);                                               \
         else ORBIT_LAUNCH(4, NB, OU);                                                              \
     } while (0)
     if (norm_bf16) {

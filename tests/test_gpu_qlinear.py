@@ -36,7 +36,7 @@ def _gpu(xc, xs, wc, wr, ba, bw, K):
 
 @pytest.mark.parametrize("M,N,K", [(1, 128, 64), (257, 384, 256), (300, 130, 512), (64, 3072, 3072),
                                    (129, 257, 13824), (5, 1, 128)])
-@pytest.mark.parametrize("ba,bw", [(4, 4), (4, 3), (4, 2), (3, 3), (2, 2), (3, 4), (2, 4)])
+@pytest.mark.parametrize("ba,bw", [(4, 4), (4, 3), (4, 2), (3, 3), (2, 2), (3, 4), (2, 4), (6, 4), (6, 3), (6, 2)])
 def test_random_codes(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
@@ -49,7 +49,7 @@ def test_random_codes(M, N, K, ba, bw):
 # shapes with at least 512 tiles of 256x256 run the large-tile kernel; these cover its ragged
 # edges in M and N, a single K-step and an odd number of K-steps
 @pytest.mark.parametrize("M,N,K", [(4133, 8061, 64), (4133, 8061, 192), (8197, 4099, 1024)])
-@pytest.mark.parametrize("ba,bw", [(4, 4), (4, 3), (2, 2), (3, 4)])
+@pytest.mark.parametrize("ba,bw", [(4, 4), (4, 3), (2, 2), (3, 4), (6, 4), (6, 2)])
 def test_random_codes_large_tiles(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
@@ -145,7 +145,7 @@ def test_c4_up_shape_sampled_rows():
     assert err <= GEMM_REL_F
 
 
-@pytest.mark.parametrize("bw,ba", [(4, 4), (3, 4), (2, 4), (3, 3)])
+@pytest.mark.parametrize("bw,ba", [(4, 4), (3, 4), (2, 4), (3, 3), (4, 6)])
 def test_end_to_end_c1(bw, ba):
     """GPU quantize (acts + weights) -> GPU GEMM against the oracle pipeline on the same bf16
     inputs.  Codes may differ only at near-ties, so the outputs must agree to within the bound on
@@ -175,5 +175,6 @@ def test_end_to_end_c1(bw, ba):
     log_stats(f"end-to-end c1 W{bw}A{ba}", rel_f_vs_oracle_pipeline=e_pipe, rel_f_vs_dense=e_dense,
               near_tie_bound_rel=bound / float(np.linalg.norm(ref_q)))
     assert diff <= bound + GEMM_REL_F * float(np.linalg.norm(ref_q))
-    band = {(4, 4): (0.11, 0.19), (3, 4): (0.17, 0.26), (2, 4): (0.31, 0.42), (3, 3): (0.22, 0.32)}[(bw, ba)]
+    band = {(4, 4): (0.11, 0.19), (3, 4): (0.17, 0.26), (2, 4): (0.31, 0.42), (3, 3): (0.22, 0.32),
+            (4, 6): (0.08, 0.13)}[(bw, ba)]
     assert band[0] < e_dense < band[1]

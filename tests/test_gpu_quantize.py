@@ -25,7 +25,7 @@ def _randn_bf16(M, K, seed, scale=1.0):
 
 @pytest.mark.parametrize("K,M", [(128, 1), (384, 3), (1024, 64), (3072, 257), (128, 1000), (16384, 5),
                                  (5120, 130), (13824, 3)])
-@pytest.mark.parametrize("bits", [2, 3, 4])
+@pytest.mark.parametrize("bits", [2, 3, 4, 6])
 @pytest.mark.parametrize("weights", [False, True])
 def test_small_shapes(K, M, bits, weights):
     X = _randn_bf16(M, K, seed=K * 7 + M)
@@ -62,7 +62,7 @@ def test_block_size_outlier_channels():
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2])
-@pytest.mark.parametrize("bits", [2, 3, 4])
+@pytest.mark.parametrize("bits", [2, 3, 4, 6])
 def test_c1_activations_full(seed, bits):
     X, _ = workloads.c1_inputs(device=DEV)
     compare_quantizer(f"c1 act seed={seed}", X, bits, seed=seed)
@@ -93,6 +93,16 @@ def test_c4_down_sampled_rows():
     compare_quantizer("c4 down act sampled", X, 4, seed=0, rows=rows)
     # and with the paper's block-size rule (512 for d = 13824)
     compare_quantizer("c4 down act sampled, h=512", X, 4, seed=0, rows=rows, h=512)
+
+
+def test_c4_up_a6_sampled_rows():
+    # the video recipe's 6-bit activations (W4A6) on the full up-projection input
+    fr, tpf, txt = 21, 30 * 52, 512
+    X = workloads.video_acts(fr * tpf, txt, 5120, 4, fr, workloads.C4.data_seed, 0, device=DEV)
+    rows = np.sort(np.random.default_rng(48).choice(X.shape[0], 2048, replace=False))
+    rows[-1] = X.shape[0] - 1
+    compare_quantizer("c4 up act sampled A6", X, 6, seed=0, rows=rows)
+    compare_quantizer("c4 up act sampled A6, h=1024", X, 6, seed=0, rows=rows, h=1024)
 
 
 def test_c4_up_paper_block_rule_sampled_rows():

@@ -32,7 +32,7 @@ def test_library_loads_and_exports_every_declared_symbol():
     assert lib.orbit_version().decode().startswith("orbitquant")
 
 
-@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5, 6])
 @pytest.mark.parametrize("d", [16, 64, 3072, 5120, 12288, 13824])
 def test_codebook_matches_oracle(bits, d):
     cb = oq.lloydmax_codebook(bits, d)

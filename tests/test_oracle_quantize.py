@@ -60,9 +60,12 @@ def test_pack_hand_computed_bytes():
     # b=3: sum_k code_k << 3k for (5,3,7,0,1,6,2,4) = 9114077 = 0x8B11DD, little-endian bytes
     p3 = oracle.pack_codes(np.array([[5, 3, 7, 0, 1, 6, 2, 4]]), 3)
     assert p3.tolist() == [[0xDD, 0x11, 0x8B]]
+    # b=6: 5 + 63<<6 + 0<<12 + 33<<18 = 0x840FC5, little-endian bytes
+    p6 = oracle.pack_codes(np.array([[5, 63, 0, 33]]), 6)
+    assert p6.tolist() == [[0xC5, 0x0F, 0x84]]
 
 
-@pytest.mark.parametrize("bits", [2, 3, 4])
+@pytest.mark.parametrize("bits", [2, 3, 4, 6])
 def test_pack_roundtrip(bits):
     rng = np.random.default_rng(bits)
     codes = rng.integers(0, 1 << bits, size=(7, 256))
@@ -144,7 +147,7 @@ def test_qlinear_with_identity_quantizer_recovers_dense_layer():
 
 
 @pytest.mark.parametrize("bw,ba,lo,hi", [(4, 4, 0.11, 0.19), (3, 4, 0.17, 0.26),
-                                         (2, 4, 0.31, 0.42), (3, 3, 0.22, 0.32)])
+                                         (2, 4, 0.31, 0.42), (3, 3, 0.22, 0.32), (4, 6, 0.08, 0.13)])
 def test_end_to_end_error_band(bw, ba, lo, hi):
     # statistical: independent Lloyd-Max quantizers of both operands give a relative
     # Frobenius error near sqrt(D_bw + D_ba) (Max's distortions), here on outlier data
