@@ -79,15 +79,18 @@ __device__ __forceinline__ void decode8_small(const Codes<BITS>& w, int g, const
     uint32_t lo, hi;
     uint32_t ce, co;  // codes k0 k2 k4 k6 and k1 k3 k5 k7, one per byte
     if constexpr (BITS == 2) {
-        const uint32_t x = w[g >> 1] >> (16 * (g & 1));      // 16 bits, code j at bits 2j
+        uint32_t xw = w[g >> 1];
+        asm volatile("" : "+v"(xw));  // as in decode8: keep the decode at its use
+        const uint32_t x = xw >> (16 * (g & 1));             // 16 bits, code j at bits 2j
         const uint32_t e = x & 0x3333u, o = (x >> 2) & 0x3333u;  // nibble i holds k2i (k2i+1)
         ce = __builtin_amdgcn_perm(e >> 4, e, 0x05010400u) & 0x03030303u;
         co = __builtin_amdgcn_perm(o >> 4, o, 0x05010400u) & 0x03030303u;
     } else {
         static_assert(BITS == 3, "bits");
         const int bit = 24 * g;                               // 24 bits, code j at bits 3j
-        const uint32_t x = bit == 0 ? w[0] : bit == 24 ? (w[0] >> 24) | (w[1] << 8)
-                         : bit == 48 ? (w[1] >> 16) | (w[2] << 16) : w[2] >> 8;
+        uint32_t x = bit == 0 ? w[0] : bit == 24 ? (w[0] >> 24) | (w[1] << 8)
+                   : bit == 48 ? (w[1] >> 16) | (w[2] << 16) : w[2] >> 8;
+        asm volatile("" : "+v"(x));  // as in decode8: keep the decode at its use
         ce = (x & 7u) | (((x >> 6) & 7u) << 8) | (((x >> 12) & 7u) << 16) | (((x >> 18) & 7u) << 24);
         co = ((x >> 3) & 7u) | (((x >> 9) & 7u) << 8) | (((x >> 15) & 7u) << 16) | (((x >> 21) & 7u) << 24);
     }
@@ -103,8 +106,9 @@ __device__ __forceinline__ void decode8_small(const Codes<BITS>& w, int g, const
 __device__ __forceinline__ void decode8_lds6(const Codes<6>& w, int g, const uint32_t* tab, uint32_t (&out)[4]) {
     // group g covers bits 48g .. 48g+47 of the 192-bit stream (selects, not an indexed load from
     // the register array)
-    const uint32_t lo = g == 0 ? w[0] : g == 1 ? w[1] : g == 2 ? w[3] : w[4];
-    const uint32_t hi = g == 0 ? w[1] : g == 1 ? w[2] : g == 2 ? w[4] : w[5];
+    uint32_t lo = g == 0 ? w[0] : g == 1 ? w[1] : g == 2 ? w[3] : w[4];
+    uint32_t hi = g == 0 ? w[1] : g == 1 ? w[2] : g == 2 ? w[4] : w[5];
+    asm volatile("" : "+v"(lo), "+v"(hi));  // as in decode8: keep the decode at its use
     const uint64_t x = (((uint64_t)hi << 32) | lo) >> ((g & 1) * 16);
     uint32_t v[8];
 #pragma unroll
@@ -126,8 +130,11 @@ __device__ __forceinline__ void decode8(const Codes<BITS>& w, int g, const ByteT
     } else if constexpr (BITS == 4) {
         // nibble j of x is code k_j; neg has bit 3 of each nibble set where that code is below 8
         // (a negative level); there the low three bits are mirrored (j -> 7 - j) to index the
-        // positive half, and the sign bit is set on the high byte afterwards
-        const uint32_t x = w[g];
+        // positive half, and the sign bit is set on the high byte afterwards.  The empty asm pins
+        // the decode here: otherwise the compiler starts it right after the codes' load, which
+        // then has to complete a whole K-step early.
+        uint32_t x = w[g];
+        asm volatile("" : "+v"(x));
         const uint32_t neg = ~x & 0x88888888u;
         const uint32_t idx = x ^ (neg - (neg >> 3));
         lookup_bytes(idx & 0x07070707u, t, lo, hi);                  // k0 k2 k4 k6
@@ -340,10 +347,29 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     }
     __syncthreads();
 
-    // One K-step: MFMAs over stage s&1 while the codes in (ca, cb) - step s+1 - are decoded into
-    // the other stage and the codes of step s+2 load into (na, nb).  The loop below is unrolled
-    // by two so that the code registers swap roles instead of being copied (a copy would wait
-    // for the load).
+    // fragments of one 16-wide k slice of a stage
+    half8 a[2][4], b[2][2];
+    auto read_frags = [&](int stage, int kk, half8 (&af)[4], half8 (&bf)[2]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) af[i] = *(const half8*)(a_frag0 + stage + i * 32 * LDS2_STRIDE + kk * 16);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) bf[j] = *(const half8*)(b_frag0 + stage + j * 32 * LDS2_STRIDE + kk * 16);
+    };
+    auto decode_group = [&](int nxt, int g, const Codes<BA>& ca, const Codes<BW>& cb) {
+        uint32_t da[4], db[4];
+        decode8<BA>(ca, g, ta, tab6, da);
+        decode8<BW>(cb, g, tw, nullptr, db);
+        *(uint4*)(a_dst0 + nxt + 8 * g) = make_uint4(da[0], da[1], da[2], da[3]);
+        *(uint4*)(a_dst0 + nxt + LDS2_TILE + 8 * g) = make_uint4(db[0], db[1], db[2], db[3]);
+    };
+    read_frags(0, 0, a[0], b[0]);
+
+    // One K-step in four 16-wide slices.  Slices 0-2 decode the codes of step s+1 (ca, cb) into
+    // the other stage while their MFMAs run; then one barrier makes that stage complete and
+    // retires every read of this step's stage, so slice 3 can already fetch the next step's
+    // first fragments while its MFMAs run.  The codes of step s+2 load into (na, nb).  The loop
+    // below is unrolled by two so that the code registers swap roles instead of being copied (a
+    // copy would wait for the load).
     auto kstep = [&](int s, const Codes<BA>& ca, const Codes<BW>& cb, Codes<BA>& na, Codes<BW>& nb) {
         // the last steps re-load the final step's codes; they are never used
         const int64_t s2 = min(s + 2, nk - 1);
@@ -352,30 +378,20 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
         __builtin_amdgcn_sched_barrier(0);
 
         const int cur = (s & 1) * STAGE, nxt = STAGE - cur;
-        half8 a[2][4], b[2][2];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) a[0][i] = *(const half8*)(a_frag0 + cur + i * 32 * LDS2_STRIDE);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) b[0][j] = *(const half8*)(b_frag0 + cur + j * 32 * LDS2_STRIDE);
 #pragma unroll
         for (int kk = 0; kk < BK2 / 16; ++kk) {
             const int f = kk & 1;
-            if (kk + 1 < BK2 / 16) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    a[f ^ 1][i] = *(const half8*)(a_frag0 + cur + i * 32 * LDS2_STRIDE + (kk + 1) * 16);
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    b[f ^ 1][j] = *(const half8*)(b_frag0 + cur + j * 32 * LDS2_STRIDE + (kk + 1) * 16);
-            }
-            // decode one group of the next step's codes into the other stage (it was last read
-            // before the previous barrier); on the final step this refills a stage nobody reads
-            {
-                uint32_t da[4], db[4];
-                decode8<BA>(ca, kk, ta, tab6, da);
-                decode8<BW>(cb, kk, tw, nullptr, db);
-                *(uint4*)(a_dst0 + nxt + 8 * kk) = make_uint4(da[0], da[1], da[2], da[3]);
-                *(uint4*)(a_dst0 + nxt + LDS2_TILE + 8 * kk) = make_uint4(db[0], db[1], db[2], db[3]);
+            if (kk == 3) __syncthreads();
+            // next slice's fragments; after the barrier, the next step's first slice (on the final
+            // step a refilled stage nobody uses)
+            if (kk < 3) read_frags(cur, kk + 1, a[f ^ 1], b[f ^ 1]);
+            else read_frags(nxt, 0, a[f ^ 1], b[f ^ 1]);
+            // decode groups 0,1 | 2 | 3 | - of the next step in slices 0 | 1 | 2 | 3
+            if (kk == 0) {
+                decode_group(nxt, 0, ca, cb);
+                decode_group(nxt, 1, ca, cb);
+            } else if (kk < 3) {
+                decode_group(nxt, kk + 1, ca, cb);
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -384,16 +400,24 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(b[f][j], a[f][i], acc[i][j], 0, 0, 0);
             // issue order inside the slice: next fragments first, then each MFMA followed by a
             // share of the decode, the decoded rows' LDS writes last
-            if (kk + 1 < BK2 / 16) __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+            if (kk == 0) {
 #pragma unroll
-            for (int m = 0; m < 8; ++m) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+                for (int m = 0; m < 8; ++m) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 4, 0);
+            } else if (kk < 3) {
+#pragma unroll
+                for (int m = 0; m < 8; ++m) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
             __builtin_amdgcn_sched_barrier(0);
         }
-        __syncthreads();
     };
 
     int s = 0;
