@@ -299,7 +299,7 @@ struct Quantizer {
         for (int i = 0; i < 16; ++i) {
             const uint32_t lo = *(const uint16_t*)(smem + addr[2 * i]);
             const uint32_t hi = *(const uint16_t*)(smem + addr[2 * i + 1]);
-            P[i] = lo | (hi << 16);
+            P[i] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);  // lo | hi << 16 in one op
         }
         u32x4 pf[4];
         if (next < p.ngroups) load_group(next, pf);
@@ -380,7 +380,7 @@ struct Quantizer {
         for (int r = r_first; r <= r_last && r < nrows; ++r) {
             float acc = 0.f;
             for (int i = lane; i < nb; i += 64) acc += part[r * nb + i];
-            const float tot = sqrtf(wave_total(acc));
+            const float tot = __builtin_amdgcn_sqrtf(wave_total(acc));  // v_sqrt_f32 (1 ulp; no scaling fixups)
             if (rg == r) s = tot;
         }
         if (owner && blk == 0 && q == 0) {
@@ -393,7 +393,7 @@ struct Quantizer {
         // u = z / (s + eps) with z = z_unnormalised / sqrt(h); t = u / w + center is the cell
         // coordinate and round(0.5 t + bias[cell]) the code
         // (the floor keeps t finite, so the table index stays in range, for any eps >= 0)
-        const float a = sigma * p.enc_inv_w / (fmaxf(s + p.eps, 1e-30f) * p.sqrt_h);
+        const float a = sigma * p.enc_inv_w * __builtin_amdgcn_rcpf(fmaxf(s + p.eps, 1e-30f) * p.sqrt_h);  // 1-ulp rcp
         const float c = p.enc_center;
         const float* tab = (const float*)(smem + kEncOff);
         float y[32];
