@@ -254,10 +254,11 @@ def main():
         pb = oq.rpbh_plan_from_arrays(K0, pr.h, np.arange(K0), signs)
         rot[f"rpbh_h{pr.h}_ms"] = time_quant(pr)
         rot[f"block_rht_h{pr.h}_ms"] = time_quant(pb)
-    gq = torch.Generator(device=dev)
+    # the Haar rotation itself is drawn on the host: only its application is timed
+    gq = torch.Generator()
     gq.manual_seed(7)
-    Q, _ = torch.linalg.qr(torch.randn((K0, K0), generator=gq, device=dev, dtype=torch.float32))
-    Qt = Q.t().contiguous().to(torch.bfloat16)
+    Q, _ = torch.linalg.qr(torch.randn((K0, K0), generator=gq, dtype=torch.float32))
+    Qt = Q.t().contiguous().to(torch.bfloat16).to(dev)
     del Q
     Xr = torch.empty((L0["lin"].M, K0), dtype=torch.bfloat16, device=dev)
     for _ in range(2):
