@@ -49,6 +49,7 @@ namespace {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kEncOff = 32768;  // byte offset of the encoder table (the row buffer comes first)
 
@@ -294,12 +295,15 @@ struct Quantizer {
         float* part = (float*)(smem + kEncOff + p.ncell * 4);
 
         // gathered pairs: element 2i in the low half, 2i+1 in the high half of P[i]
+        // (built as a two-lane vector, the pair becomes one v_perm of the two loads with no
+        // masking of the zero-extended halves)
         uint32_t P[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            const uint32_t lo = *(const uint16_t*)(smem + addr[2 * i]);
-            const uint32_t hi = *(const uint16_t*)(smem + addr[2 * i + 1]);
-            P[i] = __builtin_amdgcn_perm(hi, lo, 0x05040100u);  // lo | hi << 16 in one op
+            u16x2 v;
+            v.x = *(const uint16_t*)(smem + addr[2 * i]);
+            v.y = *(const uint16_t*)(smem + addr[2 * i + 1]);
+            P[i] = __builtin_bit_cast(uint32_t, v);
         }
         u32x4 pf[4];
         if (next < p.ngroups) load_group(next, pf);
