@@ -183,6 +183,16 @@ def c2_weights(device="cpu"):
     return up, down
 
 
+def c2_down_acts(step: int, device="cpu") -> torch.Tensor:
+    """Down-projection input at denoising step `step`: GELU (exact erf) of the unquantized
+    up-projection X_up W_up^T in fp32, rounded to BF16 (the dense layer stands in for the real
+    model's hidden activations)."""
+    Xu = c2_up_acts(step, device=device).float()
+    Wu, _ = c2_weights(device=device)
+    H = Xu @ Wu.float().t().contiguous()
+    return to_bf16(torch.nn.functional.gelu(H))
+
+
 def c3_inputs(device="cpu"):
     """(X_qkv, X_out, W_qkv, W_out) for the attention projections."""
     M, K = C3_M, 3072
