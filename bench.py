@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--workload", default="c4_video_mlp_w4a4", choices=["c4_video_mlp_w4a4", "c1_single_w4a4"])
     ap.add_argument("--cpu-baseline-rows", type=int, default=12288,
                     help="token rows of the oracle's timed CPU sample (0 disables it)")
+    ap.add_argument("--trunk-steps", type=int, default=2,
+                    help="timed steps of the 40-block video trunk sweep (config 5); 0 skips it")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device-to-device copy of this many MiB before the step, so that a "
                          "counter profile of this run holds a kernel of known traffic to scale by")
@@ -318,6 +320,10 @@ def main():
           "gemm_ms": g6_ms, "gemm_tflops": float(flops[0]) / (g6_ms * 1e-3) / 1e12}
     del xc6
 
+    trunk = None
+    if args.trunk_steps > 0:
+        trunk = trunk_sweep(oq, workloads, dev, args.trunk_steps)
+
     cpu = None
     if args.cpu_baseline_rows > 0:
         cpu = cpu_baseline(layers, args.cpu_baseline_rows)
@@ -361,10 +367,88 @@ def main():
         "rotation_classes": rot,
         "fused_epilogue": fused,
         "w4a6": a6,
+        "trunk_c5": trunk,
         "cpu_baseline": cpu,
         "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0)},
     }
     print(json.dumps(out), flush=True)
+
+
+def trunk_sweep(oq, workloads, dev, steps, warmup=1):
+    """The video-DiT trunk sweep: per denoising step, the activation quantizer and the GEMM of
+    every linear of 40 blocks (QKV, out, FFN up, FFN down at M = 32760), summed over the 160
+    calls; and the offline weight pass over all 160 weight matrices, timed launch by launch with
+    the weights' generation outside the timing.  One activation draw per input width serves every
+    block."""
+    wl = workloads.C5
+    acts = workloads.c5_acts(device=dev)
+    M = workloads.C5_M
+    plans = {K: oq.rpbh_plan(K, 128, wl.plan_seed) for K in acts}
+    cbs = {K: oq.lloydmax_codebook(4, K) for K in acts}
+    xc = {K: torch.empty((M, K // 2), dtype=torch.uint8, device=dev) for K in acts}
+    xn = {K: torch.empty((M,), dtype=torch.float32, device=dev) for K in acts}
+    Yflat = torch.empty(max(M * lin.N for lin in wl.linears), dtype=torch.float32, device=dev)
+
+    # offline weight pass, all blocks
+    wcodes, wnorms = [], []
+    wp_ms, wp_bytes, n_weights = 0.0, 0.0, 0
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for b in range(wl.repeat):
+        for li, lin in enumerate(wl.linears):
+            W = workloads.c5_weight(b, li, device=dev)
+            wc = torch.empty((lin.N, lin.K // 2), dtype=torch.uint8, device=dev)
+            wn = torch.empty((lin.N,), dtype=torch.bfloat16, device=dev)
+            torch.cuda.synchronize()
+            e0.record()
+            oq.quantize_weights_offline(plans[lin.K], cbs[lin.K], W, 1e-10, wc, wn)
+            e1.record()
+            torch.cuda.synchronize()
+            wp_ms += e0.elapsed_time(e1)
+            wp_bytes += lin.N * (2 * lin.K + lin.K // 2 + 2)
+            n_weights += lin.N * lin.K
+            wcodes.append(wc)
+            wnorms.append(wn)
+            del W
+
+    def step(ev=None):
+        for b in range(wl.repeat):
+            for li, lin in enumerate(wl.linears):
+                i = b * len(wl.linears) + li
+                if ev is not None:
+                    ev[4 * i].record()
+                oq.rpbh_quantize_act(plans[lin.K], cbs[lin.K], acts[lin.K], 1e-10, xc[lin.K], xn[lin.K])
+                if ev is not None:
+                    ev[4 * i + 1].record()
+                    ev[4 * i + 2].record()
+                oq.orbit_qlinear(cbs[lin.K], xc[lin.K], xn[lin.K], cbs[lin.K], wcodes[i], wnorms[i],
+                                 Yflat[:M * lin.N].view(M, lin.N))
+                if ev is not None:
+                    ev[4 * i + 3].record()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    n = wl.repeat * len(wl.linears)
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4 * n)] for _ in range(steps)]
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record()
+    for k in range(steps):
+        step(events[k])
+    s1.record()
+    torch.cuda.synchronize()
+    step_ms = s0.elapsed_time(s1) / steps
+    q_ms = sum(ev[4 * i].elapsed_time(ev[4 * i + 1]) for ev in events for i in range(n)) / steps
+    g_ms = sum(ev[4 * i + 2].elapsed_time(ev[4 * i + 3]) for ev in events for i in range(n)) / steps
+    flops = wl.repeat * sum(2.0 * M * lin.N * lin.K for lin in wl.linears)
+    qbytes = wl.repeat * sum(quant_bytes(M, lin.K, 4) for lin in wl.linears)
+    return {"workload": wl.name, "blocks": wl.repeat, "linears_per_step": n, "M": M, "steps": steps,
+            "step_ms": step_ms, "step_tflops": flops / (step_ms * 1e-3) / 1e12,
+            "gemm_ms_sum": g_ms, "gemm_tflops": flops / (g_ms * 1e-3) / 1e12,
+            "gemm_frac_of_fp16_peak": flops / (g_ms * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS,
+            "quant_ms_sum": q_ms, "quant_gbs": qbytes / (q_ms * 1e-3) / 1e9,
+            "quant_frac_of_hbm": qbytes / (q_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "weight_pass_ms": wp_ms, "weight_pass_gbs": wp_bytes / (wp_ms * 1e-3) / 1e9,
+            "weights": n_weights, "weight_code_bytes": int(sum(c.numel() for c in wcodes))}
 
 
 def cpu_baseline(layers, rows):

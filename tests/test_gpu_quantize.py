@@ -73,6 +73,19 @@ def test_c1_weights_full():
     compare_quantizer("c1 weights", W, 4, seed=0, weights=True)
 
 
+def test_c2_activations_every_timestep():
+    # the image MLP's up-projection input: every row at timestep 0, 256 sampled rows (the last
+    # included) at each of the other 27 steps, all with the one fixed codebook
+    T = workloads.C2.extra["timesteps"]
+    for step in range(T):
+        X = workloads.c2_up_acts(step, device=DEV)
+        rows = None
+        if step > 0:
+            rows = np.sort(np.random.default_rng(70 + step).choice(X.shape[0], 256, replace=False))
+            rows[-1] = X.shape[0] - 1
+        compare_quantizer(f"c2 up act step {step}", X, 4, seed=0, rows=rows)
+
+
 @pytest.mark.parametrize("bits", [3, 4])
 def test_c3_activations_full(bits):
     Xq, _, _, _ = workloads.c3_inputs(device=DEV)
