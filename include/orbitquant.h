@@ -145,8 +145,8 @@ void lloydmax_codebook_destroy(orbit_codebook c);
  *
  * Pointers: W and w_codes 16-byte aligned, w_norm 2-byte aligned.
  * Errors: ORBIT_EINVAL (null pointer, K mismatch, ldw, alignment); ORBIT_EUNSUPPORTED
- * (h outside 128..4096, K > 16384 or bits not in {2, 3, 4, 6}); ORBIT_EHIP.  N = 0 returns at
- * once.  Packing as above: at b = 6 every 4 codes fill 3 bytes.
+ * (h outside 128..4096, K > 16384, bits not in {2, 3, 4, 6}, more than 2^31 - 1 rows);
+ * ORBIT_EHIP.  N = 0 returns at once.  Packing as above: at b = 6 every 4 codes fill 3 bytes.
  */
 orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const uint16_t* W, int64_t N,
                                       int64_t K, int64_t ldw, float eps, uint8_t* w_codes,
@@ -189,8 +189,9 @@ orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t
  * handled element-wise).  The 4-bit decoder relies on the codebook's exact antisymmetry in
  * fp16 (L[15-c] = -L[c]), which lloydmax_codebook guarantees; ORBIT_EINTERNAL otherwise.
  * Errors: ORBIT_EINVAL (null pointer, dimension mismatch, ldy < N); ORBIT_EUNSUPPORTED
- * (activation bits not in {2, 3, 4, 6}, weight bits outside 2..4, K not a multiple of 64);
- * ORBIT_EHIP.  M = 0 or N = 0 returns at once.
+ * (activation bits not in {2, 3, 4, 6}, weight bits outside 2..4, K not a multiple of 64,
+ * M or N above 2^31 - 1 or more than 2^27 output tiles of 256 x 256); ORBIT_EHIP.  M = 0 or
+ * N = 0 returns at once.
  */
 orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
                            orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,

@@ -180,9 +180,23 @@ def code_bytes(K: int, bits: int) -> int:
 
 
 def _rows(t: torch.Tensor, name: str):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a tensor on a GPU")
     if t.dim() != 2 or t.dtype != torch.bfloat16 or t.stride(1) != 1:
         raise ValueError(f"{name} must be a 2-D bf16 tensor with contiguous rows")
     return t.shape[0], t.shape[1], t.stride(0)
+
+
+def _expect(t: torch.Tensor, name: str, dtype: torch.dtype, shape: tuple, device: torch.device):
+    """The kernels address buffers from their sizes alone, so every tensor handed to them must have
+    exactly the documented dtype and shape, dense rows, and sit on the device of the call."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the call runs on {device}")
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)}, "
+                         f"got {t.dtype} {tuple(t.shape)}{'' if t.is_contiguous() else ' (not contiguous)'}")
 
 
 def quantize_weights_offline(plan: Plan, cb_w: Codebook, W: torch.Tensor, eps: float = 1e-10,
@@ -193,8 +207,11 @@ def quantize_weights_offline(plan: Plan, cb_w: Codebook, W: torch.Tensor, eps: f
         codes = torch.empty((N, code_bytes(K, cb_w.bits)), dtype=torch.uint8, device=W.device)
     if norms is None:
         norms = torch.empty((N,), dtype=torch.bfloat16, device=W.device)
-    _check("quantize_weights_offline", lib().quantize_weights_offline(
-        plan.handle, cb_w.handle, _ptr(W), N, K, ldw, eps, _ptr(codes), _ptr(norms), _stream(W)))
+    _expect(codes, "codes", torch.uint8, (N, code_bytes(K, cb_w.bits)), W.device)
+    _expect(norms, "norms", torch.bfloat16, (N,), W.device)
+    with torch.cuda.device(W.device):
+        _check("quantize_weights_offline", lib().quantize_weights_offline(
+            plan.handle, cb_w.handle, _ptr(W), N, K, ldw, eps, _ptr(codes), _ptr(norms), _stream(W)))
     return codes, norms
 
 
@@ -206,23 +223,50 @@ def rpbh_quantize_act(plan: Plan, cb_a: Codebook, X: torch.Tensor, eps: float = 
         codes = torch.empty((M, code_bytes(K, cb_a.bits)), dtype=torch.uint8, device=X.device)
     if norms is None:
         norms = torch.empty((M,), dtype=torch.float32, device=X.device)
-    _check("rpbh_quantize_act", lib().rpbh_quantize_act(
-        plan.handle, cb_a.handle, _ptr(X), M, K, ldx, eps, _ptr(codes), _ptr(norms), _stream(X)))
+    _expect(codes, "codes", torch.uint8, (M, code_bytes(K, cb_a.bits)), X.device)
+    _expect(norms, "norms", torch.float32, (M,), X.device)
+    with torch.cuda.device(X.device):
+        _check("rpbh_quantize_act", lib().rpbh_quantize_act(
+            plan.handle, cb_a.handle, _ptr(X), M, K, ldx, eps, _ptr(codes), _ptr(norms), _stream(X)))
     return codes, norms
+
+
+def _qlinear_operands(cb_a: Codebook, x_codes, x_norm, cb_w: Codebook, w_codes, w_norm):
+    if cb_a.d != cb_w.d:
+        raise ValueError(f"codebooks are for d={cb_a.d} and d={cb_w.d}")
+    if not isinstance(x_codes, torch.Tensor) or not x_codes.is_cuda or x_codes.dim() != 2:
+        raise ValueError("x_codes must be a 2-D tensor on a GPU")
+    if not isinstance(w_codes, torch.Tensor) or w_codes.dim() != 2:
+        raise ValueError("w_codes must be a 2-D tensor")
+    K, dev = cb_a.d, x_codes.device
+    M, N = x_codes.shape[0], w_codes.shape[0]
+    _expect(x_codes, "x_codes", torch.uint8, (M, code_bytes(K, cb_a.bits)), dev)
+    _expect(x_norm, "x_norm", torch.float32, (M,), dev)
+    _expect(w_codes, "w_codes", torch.uint8, (N, code_bytes(K, cb_w.bits)), dev)
+    _expect(w_norm, "w_norm", torch.bfloat16, (N,), dev)
+    return M, N, K, dev
+
+
+def _check_out(out: torch.Tensor, M: int, N: int, dtype: torch.dtype, dev: torch.device):
+    if not isinstance(out, torch.Tensor) or out.device != dev:
+        raise ValueError(f"out must be a tensor on {dev}")
+    if out.dim() != 2 or tuple(out.shape) != (M, N) or out.stride(1) != 1 or out.dtype != dtype:
+        raise ValueError(f"out must be a 2-D {dtype} tensor of shape ({M}, {N}) with contiguous rows")
+    if M > 1 and out.stride(0) < N:
+        raise ValueError("out rows overlap (stride(0) < N)")
 
 
 def orbit_qlinear(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor, cb_w: Codebook,
                   w_codes: torch.Tensor, w_norm: torch.Tensor, out: torch.Tensor = None) -> torch.Tensor:
     """Quantized layer on codes: Y fp32 [M, N] = diag(s) La[Xc] Lw[Wc]^T diag(r')."""
-    M, N = x_codes.shape[0], w_codes.shape[0]
-    K = cb_a.d
+    M, N, K, dev = _qlinear_operands(cb_a, x_codes, x_norm, cb_w, w_codes, w_norm)
     if out is None:
-        out = torch.empty((M, N), dtype=torch.float32, device=x_codes.device)
-    if out.dim() != 2 or out.stride(1) != 1 or out.dtype != torch.float32:
-        raise ValueError("out must be a 2-D fp32 tensor with contiguous rows")
-    _check("orbit_qlinear", lib().orbit_qlinear(
-        cb_a.handle, _ptr(x_codes), _ptr(x_norm), M, cb_w.handle, _ptr(w_codes), _ptr(w_norm), N, K,
-        _ptr(out), out.stride(0), _stream(x_codes)))
+        out = torch.empty((M, N), dtype=torch.float32, device=dev)
+    _check_out(out, M, N, torch.float32, dev)
+    with torch.cuda.device(dev):
+        _check("orbit_qlinear", lib().orbit_qlinear(
+            cb_a.handle, _ptr(x_codes), _ptr(x_norm), M, cb_w.handle, _ptr(w_codes), _ptr(w_norm), N, K,
+            _ptr(out), max(out.stride(0), N), _stream(x_codes)))
     return out
 
 
@@ -230,21 +274,20 @@ def orbit_qlinear_ex(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor
                      w_codes: torch.Tensor, w_norm: torch.Tensor, bias: torch.Tensor = None, gelu: bool = False,
                      out_dtype: torch.dtype = torch.float32, out: torch.Tensor = None) -> torch.Tensor:
     """The quantized layer with bias, GELU and the output type fused into the GEMM's epilogue."""
-    M, N = x_codes.shape[0], w_codes.shape[0]
-    K = cb_a.d
+    M, N, K, dev = _qlinear_operands(cb_a, x_codes, x_norm, cb_w, w_codes, w_norm)
     if out_dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
     if out is None:
-        out = torch.empty((M, N), dtype=out_dtype, device=x_codes.device)
-    if out.dim() != 2 or out.stride(1) != 1 or out.dtype != out_dtype:
-        raise ValueError("out must be a 2-D tensor of out_dtype with contiguous rows")
-    if bias is not None and (bias.dtype != torch.bfloat16 or bias.numel() != N or not bias.is_contiguous()):
-        raise ValueError("bias must be a contiguous bf16 vector of N entries")
-    _check("orbit_qlinear_ex", lib().orbit_qlinear_ex(
-        cb_a.handle, _ptr(x_codes), _ptr(x_norm), M, cb_w.handle, _ptr(w_codes), _ptr(w_norm), N, K,
-        _ptr(bias) if bias is not None else None, ORBIT_ACT_GELU if gelu else ORBIT_ACT_NONE,
-        ORBIT_OUT_BF16 if out_dtype == torch.bfloat16 else ORBIT_OUT_F32, _ptr(out), out.stride(0),
-        _stream(x_codes)))
+        out = torch.empty((M, N), dtype=out_dtype, device=dev)
+    _check_out(out, M, N, out_dtype, dev)
+    if bias is not None:
+        _expect(bias, "bias", torch.bfloat16, (N,), dev)
+    with torch.cuda.device(dev):
+        _check("orbit_qlinear_ex", lib().orbit_qlinear_ex(
+            cb_a.handle, _ptr(x_codes), _ptr(x_norm), M, cb_w.handle, _ptr(w_codes), _ptr(w_norm), N, K,
+            _ptr(bias) if bias is not None else None, ORBIT_ACT_GELU if gelu else ORBIT_ACT_NONE,
+            ORBIT_OUT_BF16 if out_dtype == torch.bfloat16 else ORBIT_OUT_F32, _ptr(out), max(out.stride(0), N),
+            _stream(x_codes)))
     return out
 
 

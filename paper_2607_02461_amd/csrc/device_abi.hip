@@ -112,6 +112,9 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     if (K > kQuantMaxK) return fail(ORBIT_EUNSUPPORTED, "%s: K=%lld above %lld", who, (long long)K, (long long)kQuantMaxK);
     if ((int64_t)quant_rows_per_group((int)K) * ldx * 2 >= ((int64_t)1 << 31))
         return fail(ORBIT_EUNSUPPORTED, "%s: row stride %lld too large", who, (long long)ldx);
+    if (M > INT32_MAX) return fail(ORBIT_EUNSUPPORTED, "%s: M=%lld above 2^31-1 rows", who, (long long)M);
+    if (cb->enc.ncell > kQuantMaxCells)
+        return fail(ORBIT_EUNSUPPORTED, "%s: encoder table of %d cells exceeds %d", who, cb->enc.ncell, kQuantMaxCells);
     if (M == 0) return ORBIT_OK;
     if (!X || !codes || !norm) return fail(ORBIT_EINVAL, "%s: null device pointer", who);
     if (!aligned(X, 16) || !aligned(codes, 16) || !aligned(norm, norm_bf16 ? 2 : 4))
@@ -126,8 +129,6 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     const float* enc = nullptr;
     st = codebook_enc(cb, dev, &enc);
     if (st != ORBIT_OK) return st;
-    if (cb->enc.ncell > kQuantMaxCells)
-        return fail(ORBIT_EUNSUPPORTED, "%s: encoder table of %d cells exceeds %d", who, cb->enc.ncell, kQuantMaxCells);
 
     QuantParams q{};
     q.X = X;
@@ -217,6 +218,10 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
                     "orbit_qlinear: bit-widths (a %d, w %d) not implemented (activations 2, 3, 4, 6; weights 2..4)",
                     cb_a->bits, cb_w->bits);
     if (K % 64 != 0 || K > (int64_t)1 << 30) return fail(ORBIT_EUNSUPPORTED, "orbit_qlinear: K=%lld must be a multiple of 64", (long long)K);
+    // tile counts and grid sizes are 32-bit
+    if (M > INT32_MAX || N > INT32_MAX || ((M + 255) / 256) * ((N + 255) / 256) > (INT32_MAX >> 4))
+        return fail(ORBIT_EUNSUPPORTED, "orbit_qlinear: M=%lld x N=%lld exceeds the launch grid", (long long)M,
+                    (long long)N);
     if (M == 0 || N == 0) return ORBIT_OK;
     const int ysize = out_dtype == ORBIT_OUT_BF16 ? 2 : 4;
     if (!x_codes || !x_norm || !w_codes || !w_norm || !Y) return fail(ORBIT_EINVAL, "orbit_qlinear: null device pointer");

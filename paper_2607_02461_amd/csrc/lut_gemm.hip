@@ -491,14 +491,10 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
 
 template <int BA, int BW>
 hipError_t launch_big(const GemmParams& p, hipStream_t stream) {
-    static bool attr = false;
+    static std::atomic<uint64_t> attr{0};
     const size_t smem = (size_t)2 * 2 * LDS2_TILE * sizeof(_Float16) + (BA == 6 ? 64 * sizeof(uint32_t) : 0);
-    if (!attr) {
-        hipError_t e = hipFuncSetAttribute((const void*)lut_gemm_big<BA, BW>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)smem);
-        if (e != hipSuccess) return e;
-        attr = true;
-    }
+    const hipError_t e = raise_lds_limit((const void*)lut_gemm_big<BA, BW>, (int)smem, attr);
+    if (e != hipSuccess) return e;
     const int ntm = (int)((p.M + BM2 - 1) / BM2), ntn = (int)((p.N + BN2 - 1) / BN2);
     const int per_xcd = (ntm * ntn + 7) / 8;
     hipLaunchKernelGGL((lut_gemm_big<BA, BW>), dim3(per_xcd * 8), dim3(512), smem, stream, p, ntm, ntn, per_xcd);

@@ -469,13 +469,9 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
 }
 
 template <int BITS, bool NB, bool OUTER>
-void set_smem_limit() {
-    static bool done = false;
-    if (!done) {
-        (void)hipFuncSetAttribute((const void*)rpbh_quantize_kernel<BITS, NB, OUTER>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-        done = true;
-    }
+hipError_t set_smem_limit() {
+    static std::atomic<uint64_t> done{0};
+    return raise_lds_limit((const void*)rpbh_quantize_kernel<BITS, NB, OUTER>, 160 * 1024, done);
 }
 
 }  // namespace
@@ -495,7 +491,8 @@ hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, 
     const size_t smem = quant_smem_bytes(p.K, p.R, p.ncell);
 #define ORBIT_LAUNCH(B, NB, OU)                                                                    \
     do {                                                                                           \
-        set_smem_limit<B, NB, OU>();                                                               \
+        const hipError_t e = set_smem_limit<B, NB, OU>();                                          \
+        if (e != hipSuccess) return e;                                                             \
         hipLaunchKernelGGL((rpbh_quantize_kernel<B, NB, OU>), dim3(grid), dim3(threads), smem, stream, p); \
     } while (0)
 #define ORBIT_LAUNCH_BITS(NB, OU)                                                                  \

@@ -178,3 +178,30 @@ def test_end_to_end_c1(bw, ba):
     band = {(4, 4): (0.11, 0.19), (3, 4): (0.17, 0.26), (2, 4): (0.31, 0.42), (3, 3): (0.22, 0.32),
             (4, 6): (0.08, 0.13)}[(bw, ba)]
     assert band[0] < e_dense < band[1]
+
+
+def test_binding_rejects_bad_operands():
+    # operands whose sizes do not match the codebooks are refused before any launch
+    K = 256
+    cb4, cb3, cb_other = oq.lloydmax_codebook(4, K), oq.lloydmax_codebook(3, K), oq.lloydmax_codebook(4, 512)
+    xc = torch.zeros((8, K // 2), dtype=torch.uint8, device=DEV)
+    xn = torch.ones(8, device=DEV)
+    wc = torch.zeros((16, K // 2), dtype=torch.uint8, device=DEV)
+    wn = torch.ones(16, dtype=torch.bfloat16, device=DEV)
+    cases = [
+        lambda: oq.orbit_qlinear(cb4, xc[:, :100], xn, cb4, wc, wn),            # too few code bytes
+        lambda: oq.orbit_qlinear(cb4, xc, xn, cb3, wc, wn),                     # 3-bit rows are 96 bytes
+        lambda: oq.orbit_qlinear(cb4, xc, xn.double(), cb4, wc, wn),            # norm dtype
+        lambda: oq.orbit_qlinear(cb4, xc, xn[:7], cb4, wc, wn),                 # norm count
+        lambda: oq.orbit_qlinear(cb4, xc, xn, cb4, wc, wn.float()),             # r' must be bf16
+        lambda: oq.orbit_qlinear(cb4, xc, xn, cb_other, wc, wn),                # codebooks for another d
+        lambda: oq.orbit_qlinear(cb4, xc, xn, cb4, wc, wn, out=torch.empty((8, 15), device=DEV)),
+        lambda: oq.orbit_qlinear_ex(cb4, xc, xn, cb4, wc, wn, bias=torch.zeros(15, dtype=torch.bfloat16,
+                                                                                  device=DEV)),
+        lambda: oq.rpbh_quantize_act(oq.rpbh_plan(K, 128, 0), cb4, torch.zeros((8, K), dtype=torch.bfloat16,
+                                     device=DEV), codes=torch.empty((8, K // 4), dtype=torch.uint8, device=DEV)),
+    ]
+    for i, call in enumerate(cases):
+        with pytest.raises(ValueError):
+            call()
+    torch.cuda.synchronize()

@@ -160,3 +160,52 @@ def test_device_calls_validate_before_launch():
     st, _ = _status(lib.orbit_qlinear, cb4.handle, null, null, 4, cb4.handle, null, null, 0, 256, null, 0, null)
     assert st == oq.ORBIT_OK
     assert lib.orbit_last_error().decode() == ""
+
+
+def test_device_calls_reject_grids_beyond_32_bits():
+    lib = oq.lib()
+    p = oq.rpbh_plan(256, 128, 0)
+    cb = oq.lloydmax_codebook(4, 256)
+    null, fake = ctypes.c_void_p(0), ctypes.c_void_p(1 << 20)
+    st, msg = _status(lib.rpbh_quantize_act, p.handle, cb.handle, fake, 1 << 31, 256, 256, 1e-10, fake, fake, null)
+    assert st == oq.ORBIT_EUNSUPPORTED and "M=" in msg
+    st, msg = _status(lib.orbit_qlinear, cb.handle, fake, fake, 1 << 32, cb.handle, fake, fake, 16, 256, fake, 16, null)
+    assert st == oq.ORBIT_EUNSUPPORTED
+    st, msg = _status(lib.orbit_qlinear, cb.handle, fake, fake, 1 << 30, cb.handle, fake, fake, 1 << 30, 256, fake,
+                      1 << 30, null)
+    assert st == oq.ORBIT_EUNSUPPORTED and "grid" in msg
+
+
+def test_binding_rejects_host_tensors():
+    # the wrappers hand raw pointers to device kernels: tensors that are not on a GPU never get there
+    import torch
+    plan, cb = oq.rpbh_plan(256, 128, 0), oq.lloydmax_codebook(4, 256)
+    X = torch.zeros((4, 256), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        oq.rpbh_quantize_act(plan, cb, X)
+    with pytest.raises(ValueError):
+        oq.quantize_weights_offline(plan, cb, X)
+    xc, xn = torch.zeros((4, 128), dtype=torch.uint8), torch.ones(4)
+    wc, wn = torch.zeros((8, 128), dtype=torch.uint8), torch.ones(8, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        oq.orbit_qlinear(cb, xc, xn, cb, wc, wn)
+    with pytest.raises(ValueError):
+        oq.orbit_qlinear_ex(cb, xc, xn, cb, wc, wn, gelu=True)
+
+
+def test_binding_tensor_contract():
+    # the shape/dtype/layout checks every operand passes before a launch
+    import torch
+    dev = torch.device("cpu")
+    t = torch.zeros((4, 128), dtype=torch.uint8)
+    oq._expect(t, "t", torch.uint8, (4, 128), dev)
+    for bad in (t.to(torch.int16), t[:, :64], torch.zeros((128, 4), dtype=torch.uint8).t(),
+                torch.zeros((4, 129), dtype=torch.uint8), torch.zeros((5, 128), dtype=torch.uint8)):
+        with pytest.raises(ValueError):
+            oq._expect(bad, "t", torch.uint8, (4, 128), dev)
+    oq._check_out(torch.zeros((4, 10)), 4, 10, torch.float32, dev)
+    oq._check_out(torch.zeros((4, 12))[:, :10], 4, 10, torch.float32, dev)   # padded rows
+    for bad in (torch.zeros((10, 4)).t(), torch.zeros((4, 11)), torch.zeros((4, 10), dtype=torch.bfloat16),
+                torch.zeros((40,)).as_strided((4, 10), (5, 1))):              # overlapping rows
+        with pytest.raises(ValueError):
+            oq._check_out(bad, 4, 10, torch.float32, dev)
