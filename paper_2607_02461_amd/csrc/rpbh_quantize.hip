@@ -32,10 +32,13 @@
 //                a few shift-ors close the gaps, and 32 codes leave as one 4*b-byte vector store.
 // Blocks larger than 128 (h = 128 * 2^m, up to 4096): Sylvester H_h = (H_{2^m} (x) I_128)(I_{2^m} (x)
 // H_128), so after the 128-point transform the remaining m stages pair equal offsets of the 128-blocks
-// of an h-block.  The quads of an h-block are consecutive and aligned, so stage j pairs lanes 4*2^j
-// apart: ds_swizzle (xor 4, 8, 16) or ds_bpermute (xor 32) within a wave, and for h = 4096 an
-// exchange through LDS between two waves.  Each stage again leaves the upper lane's value negated,
-// which the per-lane encoder sign absorbs.
+// of an h-block.  The quads of an h-block are consecutive and aligned, so those stages pair lanes
+// of an aligned group of h/32.  Inside a 16-lane row they run on DPP alone, like the quad stages:
+// the four stages of a 16-lane group pair lanes along 1, 2, 7 and 15 (quad_perm, row_half_mirror,
+// row_mirror), a basis of the lane index bits; the output permutation this basis implies is undone
+// by where each lane stores its codes (see the lane set-up in the kernel).  Lanes 16 and 32 apart
+// pair through ds_swizzle and ds_bpermute, and for h = 4096 an exchange through LDS joins two waves.
+// Each stage again leaves the upper lane's value negated, which the per-lane encoder sign absorbs.
 // The row's squared norm is reduced deterministically: quad DPP sums, per-block partials in LDS,
 // then one wave per row.
 #include <hip/hip_runtime.h>
@@ -59,7 +62,7 @@ __device__ __forceinline__ float quad_perm(float v) {
 }
 constexpr int kQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
 
-// z[r] <- z[r] + sgn * z[r] of lane (lane ^ XOR), for XOR in {4, 8, 16, 32}
+// z[r] <- z[r] + sgn * z[r] of lane (lane ^ XOR), for XOR in {16, 32}
 // (eight registers at a time, so that the exchanges in flight need few temporaries)
 template <int XOR>
 __device__ __forceinline__ void lane_xor_stage(float (&z)[32], float sgn, int lane) {
@@ -250,6 +253,8 @@ struct Quantizer {
     bool active;         // lane owns a (row slot, block) of the group
     uint32_t addr[32];   // byte offset of each gathered element inside the staged group
     float sigma;
+    float sgn1, sgn2, sgn3, sgn4;  // +1 / -1: lower / upper partner in the in-row butterfly stages
+    int chunk;           // position (in 32-code units) of this lane's outputs in the row
     int cpr;             // 16-byte chunks per row
 
     __device__ __forceinline__ int rows_of(int g) const { return (int)min((int64_t)p.R, p.M - (int64_t)g * p.R); }
@@ -325,17 +330,25 @@ struct Quantizer {
                 z[r + s] = a - b;
             }
         }
-        const float sgn1 = (q & 1) ? -1.f : 1.f;
-        const float sgn2 = (q & 2) ? -1.f : 1.f;
-        ORBIT_DPP_FMAC16(z, 0, sgn1, "quad_perm:[1,0,3,2]");
-        ORBIT_DPP_FMAC16(z, 16, sgn1, "quad_perm:[1,0,3,2]");
-        ORBIT_DPP_FMAC16(z, 0, sgn2, "quad_perm:[2,3,0,1]");
-        ORBIT_DPP_FMAC16(z, 16, sgn2, "quad_perm:[2,3,0,1]");
+        // (for h = 128 the roles follow the quad index directly, recomputed here rather than held)
+        const float sg1 = OUTER ? sgn1 : ((q & 1) ? -1.f : 1.f);
+        const float sg2 = OUTER ? sgn2 : ((q & 2) ? -1.f : 1.f);
+        ORBIT_DPP_FMAC16(z, 0, sg1, "quad_perm:[1,0,3,2]");
+        ORBIT_DPP_FMAC16(z, 16, sg1, "quad_perm:[1,0,3,2]");
+        ORBIT_DPP_FMAC16(z, 0, sg2, "quad_perm:[2,3,0,1]");
+        ORBIT_DPP_FMAC16(z, 16, sg2, "quad_perm:[2,3,0,1]");
         if constexpr (OUTER) {
-            // stages across the 128-blocks of an h-block; lane bit 2+j of the quad pairs it
+            // stages across the 128-blocks of an h-block: inside a 16-lane row along 7 and 15
+            // (DPP mirrors), then lanes 16 and 32 apart
             const int lane = tid & 63, task = tid >> 2;
-            if (p.outer > 0) lane_xor_stage<4>(z, (task & 1) ? -1.f : 1.f, lane);
-            if (p.outer > 1) lane_xor_stage<8>(z, (task & 2) ? -1.f : 1.f, lane);
+            if (p.outer > 0) {
+                ORBIT_DPP_FMAC16(z, 0, sgn3, "row_half_mirror");
+                ORBIT_DPP_FMAC16(z, 16, sgn3, "row_half_mirror");
+            }
+            if (p.outer > 1) {
+                ORBIT_DPP_FMAC16(z, 0, sgn4, "row_mirror");
+                ORBIT_DPP_FMAC16(z, 16, sgn4, "row_mirror");
+            }
             if (p.outer > 2) lane_xor_stage<16>(z, (task & 4) ? -1.f : 1.f, lane);
             if (p.outer > 3) lane_xor_stage<32>(z, (task & 8) ? -1.f : 1.f, lane);
         }
@@ -409,7 +422,7 @@ struct Quantizer {
         uint32_t w[6];
         pack_codes<BITS>(y, w);
         if (owner)
-            store_packed<BITS>(p.codes + (row0 + rg) * ((int64_t)p.K * BITS / 8) + (int64_t)(blk * 4 + q) * 4 * BITS, w);
+            store_packed<BITS>(p.codes + (row0 + rg) * ((int64_t)p.K * BITS / 8) + (int64_t)(OUTER ? chunk : blk * 4 + q) * 4 * BITS, w);
         if (next < p.ngroups) {
             store_group(next, pf);
             __syncthreads();
@@ -431,11 +444,34 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
     Q.rg = task / p.nb;
     Q.blk = task - Q.rg * p.nb;
     Q.cpr = p.K >> 3;
-    Q.sigma = ((Q.q & 1) ? -1.f : 1.f) * ((Q.q & 2) ? -1.f : 1.f);
-    if constexpr (OUTER) {
-        // one more negation per stage across blocks in which this lane is the upper partner
-        for (int j = 0; j < p.outer; ++j)
-            if ((task >> j) & 1) Q.sigma = -Q.sigma;
+    {
+        // Butterflies inside a 16-lane row pair lane j with j ^ v for v = 1, 2 (quad_perm), 7
+        // (row_half_mirror) and 15 (row_mirror), as many as the h-block spans: 2 for h = 128, 3
+        // for 256, 4 from 512 up.  Stages along a basis v_k whose lower / upper roles follow the
+        // dual basis s_k (parity of s_k & v_m is 1 iff k = m) compute the Sylvester transform with
+        // its outputs permuted: lane j ends with the output at position M(j), the XOR of the s_k
+        // for which s_k & j has odd parity, so it stores its codes there.  As in every stage the
+        // upper partner's value comes out negated; sigma collects those signs.
+        const int nd = OUTER ? (p.outer == 1 ? 3 : p.outer >= 2 ? 4 : 2) : 2;
+        const int s1 = nd == 2 ? 1 : 5, s2 = nd == 2 ? 2 : 6, s3 = nd == 3 ? 4 : 12, s4 = 8;
+        const int jj = Q.tid & ((1 << nd) - 1);
+        auto odd = [](int v) { return (__popc(v) & 1) != 0; };
+        Q.sgn1 = odd(jj & s1) ? -1.f : 1.f;
+        Q.sgn2 = odd(jj & s2) ? -1.f : 1.f;
+        Q.sgn3 = odd(jj & s3) ? -1.f : 1.f;
+        Q.sgn4 = odd(jj & s4) ? -1.f : 1.f;
+        int m = (odd(jj & s1) ? s1 : 0) ^ (odd(jj & s2) ? s2 : 0);
+        if (nd > 2 && odd(jj & s3)) m ^= s3;
+        if (nd > 3 && odd(jj & s4)) m ^= s4;
+        Q.chunk = ((Q.blk * 4 + Q.q) & ~((1 << nd) - 1)) | m;
+        const int sx = s1 ^ s2 ^ (nd > 2 ? s3 : 0) ^ (nd > 3 ? s4 : 0);
+        Q.sigma = odd(jj & sx) ? -1.f : 1.f;
+        if constexpr (OUTER) {
+            // one more negation per stage across rows and waves (lanes 16, 32, 64 apart) in which
+            // this lane is the upper partner
+            for (int j = 2; j < p.outer; ++j)
+                if ((task >> j) & 1) Q.sigma = -Q.sigma;
+        }
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
