@@ -46,9 +46,10 @@ def test_random_codes(M, N, K, ba, bw):
     assert err <= GEMM_REL_F
 
 
-# shapes with at least 512 tiles of 256x256 run the large-tile kernel; these cover its ragged
-# edges in M and N, a single K-step and an odd number of K-steps
-@pytest.mark.parametrize("M,N,K", [(4133, 8061, 64), (4133, 8061, 192), (8197, 4099, 1024)])
+# shapes with at least one 256x256 tile per compute unit (256) run the large-tile kernel; these
+# cover its ragged edges in M and N, a single K-step, an odd number of K-steps and a grid of
+# under two tiles per compute unit (289)
+@pytest.mark.parametrize("M,N,K", [(4133, 8061, 64), (4133, 8061, 192), (8197, 4099, 1024), (4133, 4099, 320)])
 @pytest.mark.parametrize("ba,bw", [(4, 4), (4, 3), (2, 2), (3, 4), (6, 4), (6, 2)])
 def test_random_codes_large_tiles(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
