@@ -216,13 +216,23 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    for (int k0 = 0; k0 < p.K; k0 += BK) {
-        Codes<BA> wa;
-        Codes<BW> wb;
-        load_codes32<BA>(asrc + (int64_t)k0 * BA / 8, wa);
-        load_codes32<BW>(bsrc + (int64_t)k0 * BW / 8, wb);
-        uint4* adst = (uint4*)(As + lr * LDS_STRIDE + lh * 32);
-        uint4* bdst = (uint4*)(Bs + lr * LDS_STRIDE + lh * 32);
+    // The codes of the next D K-steps are in flight while a step is decoded and contracted: on
+    // small grids each workgroup's time is its chain of K-steps, which would otherwise wait for
+    // one global load per step.  The ring is unrolled so that every slot is a fixed register set.
+    constexpr int D = 4;  // the ring's slots (unrolled below)
+    const int nk = p.K / BK;
+    const int64_t astep = BK * BA / 8, bstep = BK * BW / 8;
+    Codes<BA> ca[D];
+    Codes<BW> cb[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        const int64_t s = min(d, nk - 1);
+        load_codes32<BA>(asrc + s * astep, ca[d]);
+        load_codes32<BW>(bsrc + s * bstep, cb[d]);
+    }
+    uint4* const adst = (uint4*)(As + lr * LDS_STRIDE + lh * 32);
+    uint4* const bdst = (uint4*)(Bs + lr * LDS_STRIDE + lh * 32);
+    auto step = [&](int s, Codes<BA>& wa, Codes<BW>& wb) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             uint32_t da[4], db[4];
@@ -230,6 +240,12 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
             decode8<BW>(wb, g, tw, nullptr, db);
             adst[g] = make_uint4(da[0], da[1], da[2], da[3]);
             bdst[g] = make_uint4(db[0], db[1], db[2], db[3]);
+        }
+        {
+            // this slot's next codes (the last steps re-load the final step's, never used)
+            const int64_t sn = min(s + D, nk - 1);
+            load_codes32<BA>(asrc + sn * astep, wa);
+            load_codes32<BW>(bsrc + sn * bstep, wb);
         }
         __syncthreads();
 #pragma unroll
@@ -248,7 +264,19 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
         __syncthreads();
+    };
+    // whole rounds of the ring without branches (so each decode waits only for its own slot's
+    // load), then the 0-3 remaining steps
+    int s = 0;
+    for (; s + D <= nk; s += D) {
+        step(s, ca[0], cb[0]);
+        step(s + 1, ca[1], cb[1]);
+        step(s + 2, ca[2], cb[2]);
+        step(s + 3, ca[3], cb[3]);
     }
+    if (s < nk) step(s, ca[0], cb[0]);
+    if (s + 1 < nk) step(s + 1, ca[1], cb[1]);
+    if (s + 2 < nk) step(s + 2, ca[2], cb[2]);
 
     // epilogue: acc element e of a 32x32 tile sits at row 8*(e/4) + 4*(lane/32) + e%4, col lane%32
 #pragma unroll
