@@ -163,14 +163,10 @@ def main():
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
 
-    quant_ms = np.zeros(nl)
-    gemm_ms = np.zeros(nl)
-    for ev in events:
-        for i in range(nl):
-            quant_ms[i] += ev[4 * i].elapsed_time(ev[4 * i + 1])
-            gemm_ms[i] += ev[4 * i + 2].elapsed_time(ev[4 * i + 3])
-    quant_ms /= args.steps
-    gemm_ms /= args.steps
+    q_all = np.array([[ev[4 * i].elapsed_time(ev[4 * i + 1]) for i in range(nl)] for ev in events])
+    g_all = np.array([[ev[4 * i + 2].elapsed_time(ev[4 * i + 3]) for i in range(nl)] for ev in events])
+    quant_ms = q_all.mean(axis=0)
+    gemm_ms = g_all.mean(axis=0)
 
     flops = np.array([2.0 * L["lin"].M * L["lin"].N * L["lin"].K for L in layers])
     qbytes = np.array([quant_bytes(L["lin"].M, L["lin"].K, L["lin"].ba) for L in layers], dtype=np.float64)
@@ -348,6 +344,8 @@ def main():
                          "bits": f"W{L['lin'].bw}A{L['lin'].ba}", "h": L["lin"].h} for L in layers],
             "value_is": "GEMM flops of the step / step time (quantizer + GEMM per linear)",
             "arith": "quantizer fp32; GEMM fp16 MFMA operands, fp32 accumulate",
+            # inputs above the 256 MB Infinity Cache stream from HBM on every step
+            "cache": "cold" if min(L["X"].numel() * 2 for L in layers) > (256 << 20) else "warm",
         },
         "components": {
             "orbit_qlinear_tflops": gemm_tflops,
@@ -356,6 +354,10 @@ def main():
             "rpbh_quantize_act_frac_of_hbm": quant_gbs / HBM_PEAK_GBS,
             "quant_ms": [float(v) for v in quant_ms],
             "gemm_ms": [float(v) for v in gemm_ms],
+            "quant_ms_median": [float(v) for v in np.median(q_all, axis=0)],
+            "quant_ms_min": [float(v) for v in q_all.min(axis=0)],
+            "gemm_ms_median": [float(v) for v in np.median(g_all, axis=0)],
+            "gemm_ms_min": [float(v) for v in g_all.min(axis=0)],
             "weight_pass_ms": weight_pass_ms,
             "weight_pass_gbs": weight_bytes / (weight_pass_ms * 1e-3) / 1e9,
             "host_plan_codebook_s": host_offline_s,
@@ -369,7 +371,10 @@ def main():
         "w4a6": a6,
         "trunk_c5": trunk,
         "cpu_baseline": cpu,
-        "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0)},
+        "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0),
+                "arch": torch.cuda.get_device_properties(0).gcnArchName,
+                "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,
+                "memory_gib": torch.cuda.get_device_properties(0).total_memory / 2 ** 30},
     }
     print(json.dumps(out), flush=True)
 

@@ -1,0 +1,33 @@
+"""bench.py's command-line contract on the CPU: it refuses more than one GPU with a one-line
+JSON message, and reports the absence of a GPU instead of falling back to anything."""
+
+import json
+import os
+import subprocess
+import sys
+
+import torch
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _run(*args):
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *args], capture_output=True, text=True,
+                       timeout=300, cwd=ROOT)
+    lines = [l for l in r.stdout.splitlines() if l.strip()]
+    return r.returncode, lines
+
+
+def test_more_than_one_gpu_is_refused():
+    rc, lines = _run("--gpus", "2", "--steps", "1", "--warmup", "0")
+    assert rc == 2 and len(lines) == 1
+    msg = json.loads(lines[0])
+    assert "error" in msg and "one GPU" in msg["error"]
+
+
+def test_no_gpu_is_reported_not_emulated():
+    if torch.cuda.is_available():
+        return
+    rc, lines = _run("--steps", "1", "--warmup", "0")
+    assert rc == 2 and len(lines) == 1
+    assert json.loads(lines[0]) == {"error": "no GPU visible"}
