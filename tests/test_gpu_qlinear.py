@@ -208,3 +208,42 @@ def test_binding_rejects_bad_operands():
         with pytest.raises(ValueError):
             call()
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("ba,bw", [(4, 4), (2, 3)])
+def test_long_contraction(ba, bw):
+    # K = 65536 (1024 K-steps of fp32 accumulation) on the 128 x 128 kernel, all outputs
+    M, N, K = 300, 260, 65536
+    xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=K + ba)
+    Y = _gpu(xc, xs, wc, wr, ba, bw, K)
+    ref = qlinear_oracle_fp16(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
+    err = rel_frobenius(Y, ref)
+    log_stats(f"gemm long K={K} W{bw}A{ba}", rel_f=err)
+    assert err <= GEMM_REL_F
+
+
+def test_long_contraction_large_tiles_sampled_rows():
+    # K = 16384 (256 K-steps) on the 256 x 256 kernel (289 tiles, ragged), 64 sampled rows x all N
+    M, N, K, ba, bw = 4133, 4099, 16384, 4, 4
+    xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=7)
+    Y = _gpu(xc, xs, wc, wr, ba, bw, K)
+    rows = np.sort(np.random.default_rng(9).choice(M, 64, replace=False))
+    rows[-1] = M - 1
+    ref = qlinear_oracle_fp16(xc.numpy()[rows], xs.double().numpy()[rows], ba, wc.numpy(), wr.double().numpy(), bw, K)
+    err = rel_frobenius(Y[rows], ref)
+    log_stats(f"gemm long large-tile K={K}", rel_f=err, rows=len(rows))
+    assert err <= GEMM_REL_F
+
+
+def test_empty_operands_are_noops():
+    K = 256
+    cb = oq.lloydmax_codebook(4, K)
+    xc = torch.zeros((0, K // 2), dtype=torch.uint8, device=DEV)
+    xn = torch.zeros((0,), device=DEV)
+    wc = torch.zeros((16, K // 2), dtype=torch.uint8, device=DEV)
+    wn = torch.ones(16, dtype=torch.bfloat16, device=DEV)
+    assert oq.orbit_qlinear(cb, xc, xn, cb, wc, wn).shape == (0, 16)
+    xc1, xn1 = torch.zeros((8, K // 2), dtype=torch.uint8, device=DEV), torch.ones(8, device=DEV)
+    Y = oq.orbit_qlinear_ex(cb, xc1, xn1, cb, wc[:0], wn[:0], gelu=True, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    assert Y.shape == (8, 0)
