@@ -9,6 +9,7 @@ OrbitQuant (arXiv 2607.02461), written from the paper's definitions:
   rpbh.py      RPBH forward / inverse transform           Sec. 4.4, Eq. (9); Suppl. A setup
   quantize.py  normalize + nearest-centroid encode + pack Eqs. (5)-(8), Alg. 1
   qlinear.py   contraction of the two code sets           Sec. 4.3 (rotation cancellation)
+  adaln_rtn.py INT4 RTN g64 weight-only AdaLN projection  Sec. 5 setup; Suppl. layer list; Sec. 6.2
 
 Only the tests, the package's smoke check and the benchmark's CPU-baseline leg
 may import this package.  The product path (the HIP library and its binding)
@@ -28,6 +29,7 @@ from .rpbh import rpbh_forward, rpbh_inverse, sylvester_hadamard, fwht_blocks
 from .quantize import (normalize_rows, encode, decode_levels, pack_codes, unpack_codes,
                        quantize_act, quantize_weights, near_tie_mask, bf16_round, fp16_round)
 from .qlinear import layer_epilogue, qlinear, qlinear_dense_reference
+from .adaln_rtn import rtn_int4_quantize, rtn_int4_dequantize, pack_rtn_int4, unpack_rtn_int4, rtn_int4_linear
 
 EPS_DEFAULT = 1e-10  # Sec. 4.3: the clamp guarding zero-norm (padding) tokens
 
@@ -38,4 +40,5 @@ __all__ = [
     "normalize_rows", "encode", "decode_levels", "pack_codes", "unpack_codes",
     "quantize_act", "quantize_weights", "near_tie_mask", "bf16_round", "fp16_round",
     "qlinear", "qlinear_dense_reference", "EPS_DEFAULT",
+    "rtn_int4_quantize", "rtn_int4_dequantize", "pack_rtn_int4", "unpack_rtn_int4", "rtn_int4_linear",
 ]
