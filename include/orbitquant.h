@@ -220,6 +220,53 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
                               int64_t K, const uint16_t* bias, int32_t act, int32_t out_dtype, void* Y,
                               int64_t ldy, void* stream);
 
+/*
+ * adaln_int4_quantize_weights -- the offline pass of the adjacent layer type: the adaptive-layer-
+ * norm modulation projections, which the paper keeps at INT4 weight round-to-nearest with group
+ * size 64 and BF16 activations, unrotated (Sec. 5 setup; supplementary layer list; Sec. 6.2
+ * ablates the bit-width).  Symmetric per group of 64 consecutive inputs:
+ *     scale = fp16(min(absmax / 7, 65504)),  q = clamp(RNE(w / scale), -8, 7)
+ * with both quotients formed in fp32 (IEEE, round to nearest even); a group whose scale is 0
+ * has codes 0.
+ *
+ *   W       device, bf16 [N][ldw], the projection's weight rows
+ *   N, K    rows and inputs; K a positive multiple of 64
+ *   ldw     row stride of W in elements, >= K and a multiple of 8
+ *   q       device, uint8 [N][K/2]: q + 8 (offset binary) per nibble, element 2j in the low
+ *           nibble of byte j
+ *   scales  device, fp16 [N][K/64]
+ *   stream  hipStream_t
+ *
+ * Pointers: W and q 16-byte aligned, scales 2-byte aligned.  Errors: ORBIT_EINVAL (null pointer,
+ * K, ldw, alignment); ORBIT_EUNSUPPORTED (N above 2^31 - 1 or K above 2^30); ORBIT_EHIP.
+ * N = 0 returns at once.
+ */
+orbit_status adaln_int4_quantize_weights(const uint16_t* W, int64_t N, int64_t K, int64_t ldw, uint8_t* q,
+                                         uint16_t* scales, void* stream);
+
+/*
+ * adaln_int4_linear -- the AdaLN modulation projection on its INT4 weights:
+ *     Y[m][n] = sum_k X[m][k] * q[n][k] * scale[n][k/64] (+ bias[n])
+ * Products of the BF16 activations with the codes are exact in fp32; each group's partial sum
+ * accumulates in fp32 and is scaled before it joins the row total.  Built for the layer's shape:
+ * a few conditioning tokens (M small) against many output rows, so it streams the weights once
+ * and is bound by HBM.
+ *
+ *   X       device, bf16 [M][ldx]; ldx >= K and a multiple of 8; K <= 16384 (the tokens are
+ *           staged in LDS)
+ *   M       tokens; 0 <= M <= 131070 (rows are processed two at a time per weight pass)
+ *   q, scales, N, K   as produced by adaln_int4_quantize_weights
+ *   bias    device, bf16 [N], or NULL
+ *   Y       device, fp32 [M][ldy], ldy >= N
+ *   stream  hipStream_t
+ *
+ * Pointers: X and q 16-byte aligned; scales, bias 2-byte and Y 4-byte aligned.  Errors:
+ * ORBIT_EINVAL (null pointer, K, strides, alignment); ORBIT_EUNSUPPORTED (sizes above the
+ * limits); ORBIT_EHIP.  M = 0 or N = 0 returns at once.
+ */
+orbit_status adaln_int4_linear(const uint16_t* X, int64_t M, int64_t ldx, const uint8_t* q, const uint16_t* scales,
+                               int64_t N, int64_t K, const uint16_t* bias, float* Y, int64_t ldy, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -46,6 +46,9 @@ SIGNATURES = {
     "orbit_qlinear_ex": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
                                         _c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _c_void_p, _i64,
                                         _c_void_p]),
+    "adaln_int4_quantize_weights": (ctypes.c_int, [_c_void_p, _i64, _i64, _i64, _c_void_p, _c_void_p, _c_void_p]),
+    "adaln_int4_linear": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _i64, _i64, _c_void_p,
+                                         _c_void_p, _i64, _c_void_p]),
 }
 
 ORBIT_ACT_NONE, ORBIT_ACT_GELU = 0, 1
@@ -291,6 +294,45 @@ def orbit_qlinear_ex(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor
     return out
 
 
-__all__ = ["rpbh_plan", "rpbh_plan_from_arrays", "lloydmax_codebook", "quantize_weights_offline",
+def adaln_int4_quantize_weights(W: torch.Tensor, q: torch.Tensor = None, scales: torch.Tensor = None):
+    """Offline INT4 round-to-nearest of an AdaLN modulation projection (group 64): returns
+    (q uint8 [N, K/2] with code + 8 per nibble, scales fp16 [N, K/64])."""
+    N, K, ldw = _rows(W, "W")
+    if K % 64:
+        raise ValueError("K must be a multiple of 64")
+    if q is None:
+        q = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
+    if scales is None:
+        scales = torch.empty((N, K // 64), dtype=torch.float16, device=W.device)
+    _expect(q, "q", torch.uint8, (N, K // 2), W.device)
+    _expect(scales, "scales", torch.float16, (N, K // 64), W.device)
+    with torch.cuda.device(W.device):
+        _check("adaln_int4_quantize_weights", lib().adaln_int4_quantize_weights(
+            _ptr(W), N, K, ldw, _ptr(q), _ptr(scales), _stream(W)))
+    return q, scales
+
+
+def adaln_int4_linear(X: torch.Tensor, q: torch.Tensor, scales: torch.Tensor, bias: torch.Tensor = None,
+                      out: torch.Tensor = None) -> torch.Tensor:
+    """The AdaLN modulation projection on INT4 weights: Y fp32 [M, N] = X (q * scale)^T (+ bias)."""
+    M, K, ldx = _rows(X, "X")
+    if K % 64 or not isinstance(q, torch.Tensor) or q.dim() != 2:
+        raise ValueError("K must be a multiple of 64 and q a 2-D tensor")
+    N, dev = q.shape[0], X.device
+    _expect(q, "q", torch.uint8, (N, K // 2), dev)
+    _expect(scales, "scales", torch.float16, (N, K // 64), dev)
+    if bias is not None:
+        _expect(bias, "bias", torch.bfloat16, (N,), dev)
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=dev)
+    _check_out(out, M, N, torch.float32, dev)
+    with torch.cuda.device(dev):
+        _check("adaln_int4_linear", lib().adaln_int4_linear(
+            _ptr(X), M, ldx, _ptr(q), _ptr(scales), N, K, _ptr(bias) if bias is not None else None,
+            _ptr(out), max(out.stride(0), N), _stream(X)))
+    return out
+
+
+__all__ = ["adaln_int4_quantize_weights", "adaln_int4_linear", "rpbh_plan", "rpbh_plan_from_arrays", "lloydmax_codebook", "quantize_weights_offline",
            "rpbh_quantize_act", "orbit_qlinear", "orbit_qlinear_ex", "Plan", "Codebook", "OrbitError", "lib", "LIB_PATH",
            "SIGNATURES", "code_bytes"]

@@ -65,4 +65,21 @@ struct GemmParams {
 
 hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, int cus, hipStream_t stream);
 
+// INT4 round-to-nearest (group 64) weight-only layer of the AdaLN modulation projections.
+struct RtnLinearParams {
+    const uint16_t* X;       // bf16 [M][ldx]
+    int64_t M, ldx;
+    const uint8_t* q;        // [N][K/2]: code + 8 per nibble, LSB-first
+    const uint16_t* scales;  // fp16 [N][K/64]
+    int64_t N;
+    int K;
+    const uint16_t* bias;    // bf16 [N] or null
+    float* Y;                // fp32 [M][ldy]
+    int64_t ldy;
+};
+
+hipError_t launch_adaln_int4_quantize(const uint16_t* W, int64_t N, int K, int64_t ldw, uint8_t* q, uint16_t* scales,
+                                      hipStream_t stream);
+hipError_t launch_adaln_int4_linear(const RtnLinearParams& p, int cus, hipStream_t stream);
+
 }  // namespace orbit

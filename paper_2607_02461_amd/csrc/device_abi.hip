@@ -260,6 +260,61 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
     return ORBIT_OK;
 }
 
+orbit_status adaln_int4_quantize_weights(const uint16_t* W, int64_t N, int64_t K, int64_t ldw, uint8_t* q,
+                                         uint16_t* scales, void* stream) {
+    clear_error();
+    if (N < 0) return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: negative N");
+    if (K <= 0 || K % 64 != 0) return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: K=%lld must be a positive multiple of 64", (long long)K);
+    if (ldw < K || ldw % 8 != 0) return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: ldw=%lld must be >= K and a multiple of 8", (long long)ldw);
+    if (K > (int64_t)1 << 30 || N > INT32_MAX) return fail(ORBIT_EUNSUPPORTED, "adaln_int4_quantize_weights: N or K too large");
+    if (N == 0) return ORBIT_OK;
+    if (!W || !q || !scales) return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: null device pointer");
+    if (!aligned(W, 16) || !aligned(q, 16) || !aligned(scales, 2))
+        return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: misaligned pointer (W and q need 16 bytes)");
+    int dev;
+    DeviceInfo info;
+    orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    hipError_t e = launch_adaln_int4_quantize(W, N, (int)K, ldw, q, scales, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "adaln_int4_quantize_weights");
+    return ORBIT_OK;
+}
+
+orbit_status adaln_int4_linear(const uint16_t* X, int64_t M, int64_t ldx, const uint8_t* q, const uint16_t* scales,
+                               int64_t N, int64_t K, const uint16_t* bias, float* Y, int64_t ldy, void* stream) {
+    clear_error();
+    if (M < 0 || N < 0) return fail(ORBIT_EINVAL, "adaln_int4_linear: negative M or N");
+    if (K <= 0 || K % 64 != 0) return fail(ORBIT_EINVAL, "adaln_int4_linear: K=%lld must be a positive multiple of 64", (long long)K);
+    if (ldx < K || ldx % 8 != 0) return fail(ORBIT_EINVAL, "adaln_int4_linear: ldx=%lld must be >= K and a multiple of 8", (long long)ldx);
+    if (ldy < N) return fail(ORBIT_EINVAL, "adaln_int4_linear: ldy=%lld < N=%lld", (long long)ldy, (long long)N);
+    // the activations of two tokens are staged in LDS: K up to 16384
+    if (K > 16384 || N > INT32_MAX || M > 65535 * 2)
+        return fail(ORBIT_EUNSUPPORTED, "adaln_int4_linear: M=%lld, N=%lld or K=%lld too large", (long long)M,
+                    (long long)N, (long long)K);
+    if (M == 0 || N == 0) return ORBIT_OK;
+    if (!X || !q || !scales || !Y) return fail(ORBIT_EINVAL, "adaln_int4_linear: null device pointer");
+    if (!aligned(X, 16) || !aligned(q, 16) || !aligned(scales, 2) || !aligned(Y, 4) || (bias && !aligned(bias, 2)))
+        return fail(ORBIT_EINVAL, "adaln_int4_linear: misaligned pointer (X and q need 16 bytes)");
+    int dev;
+    DeviceInfo info;
+    orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    RtnLinearParams r{};
+    r.X = X;
+    r.M = M;
+    r.ldx = ldx;
+    r.q = q;
+    r.scales = scales;
+    r.N = N;
+    r.K = (int)K;
+    r.bias = bias;
+    r.Y = Y;
+    r.ldy = ldy;
+    hipError_t e = launch_adaln_int4_linear(r, info.cus, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "adaln_int4_linear");
+    return ORBIT_OK;
+}
+
 orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
                            orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N, int64_t K,
                            float* Y, int64_t ldy, void* stream) {

@@ -90,6 +90,26 @@ C5 = Workload(
 
 WORKLOADS = {w.name: w for w in (C1, C2, C3, C4, C5)}
 
+# The adjacent layer type: the AdaLN modulation projections of the image DiT (FLUX-shaped,
+# hidden 3072), kept at INT4 weight round-to-nearest with BF16 activations.  Each of the 19
+# double-stream blocks has two (image and text stream) of 3072 -> 6 x 3072; each of the 38
+# single-stream blocks one of 3072 -> 3 x 3072: 3.2e9 weights, the share of the model the paper
+# gives for these layers.  The input is one conditioning token per step.
+ADALN_K = 3072
+ADALN_LAYERS = ((18432, 2 * 19), (9216, 38))   # (N, count)
+ADALN_SEED = 6
+
+
+def adaln_weights(N: int, index: int, device="cpu") -> torch.Tensor:
+    """Weights of AdaLN projection `index` with N outputs: N(0, 0.02^2), BF16."""
+    return gaussian_weights(N, ADALN_K, 0.02, ADALN_SEED, index, device=device)
+
+
+def adaln_tokens(M: int, K: int = ADALN_K, seed: int = ADALN_SEED, device="cpu") -> torch.Tensor:
+    """Conditioning tokens: SiLU of N(0, 1) draws (the modulation MLP's input activation), BF16."""
+    g = _gen(seed, 701, M, device=device)
+    return to_bf16(torch.nn.functional.silu(_randn((M, K), g, device)))
+
 
 # --- helpers ----------------------------------------------------------------------------------
 def _gen(seed: int, *stream: int, device="cpu") -> torch.Generator:

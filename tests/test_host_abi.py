@@ -209,3 +209,28 @@ def test_binding_tensor_contract():
                 torch.zeros((40,)).as_strided((4, 10), (5, 1))):              # overlapping rows
         with pytest.raises(ValueError):
             oq._check_out(bad, 4, 10, torch.float32, dev)
+
+
+def test_adaln_calls_validate_before_launch():
+    lib = oq.lib()
+    null, fake = ctypes.c_void_p(0), ctypes.c_void_p(1 << 20)
+    cases = [
+        (lib.adaln_int4_quantize_weights, (fake, 4, 100, 104, fake, fake, null), oq.ORBIT_EINVAL),   # K % 64
+        (lib.adaln_int4_quantize_weights, (fake, 4, 128, 100, fake, fake, null), oq.ORBIT_EINVAL),   # ldw < K
+        (lib.adaln_int4_quantize_weights, (fake, -1, 128, 128, fake, fake, null), oq.ORBIT_EINVAL),
+        (lib.adaln_int4_quantize_weights, (null, 4, 128, 128, fake, fake, null), oq.ORBIT_EINVAL),
+        (lib.adaln_int4_quantize_weights, (ctypes.c_void_p((1 << 20) + 8), 4, 128, 128, fake, fake, null),
+         oq.ORBIT_EINVAL),                                                                            # misaligned W
+        (lib.adaln_int4_linear, (fake, 2, 128, fake, fake, 16, 96, null, fake, 16, null), oq.ORBIT_EINVAL),
+        (lib.adaln_int4_linear, (fake, 2, 120, fake, fake, 16, 128, null, fake, 16, null), oq.ORBIT_EINVAL),
+        (lib.adaln_int4_linear, (fake, 2, 128, fake, fake, 16, 128, null, fake, 8, null), oq.ORBIT_EINVAL),
+        (lib.adaln_int4_linear, (fake, 2, 128, null, fake, 16, 128, null, fake, 16, null), oq.ORBIT_EINVAL),
+        (lib.adaln_int4_linear, (fake, 1 << 20, 128, fake, fake, 16, 128, null, fake, 16, null),
+         oq.ORBIT_EUNSUPPORTED),
+    ]
+    for fn, args, want in cases:
+        st, msg = _status(fn, *args)
+        assert st == want, (fn.__name__, args, st, msg)
+    # empty calls succeed without touching the device
+    assert _status(lib.adaln_int4_linear, null, 0, 128, null, null, 16, 128, null, null, 16, null)[0] == oq.ORBIT_OK
+    assert _status(lib.adaln_int4_quantize_weights, null, 0, 128, 128, null, null, null)[0] == oq.ORBIT_OK
