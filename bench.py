@@ -40,6 +40,8 @@ def parse():
                     help="token rows of the oracle's timed CPU sample (0 disables it)")
     ap.add_argument("--trunk-steps", type=int, default=2,
                     help="timed steps of the 40-block video trunk sweep (config 5); 0 skips it")
+    ap.add_argument("--adaln-steps", type=int, default=10,
+                    help="timed steps of the AdaLN INT4 modulation projections (FLUX-shaped); 0 skips them")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device-to-device copy of this many MiB before the step, so that a "
                          "counter profile of this run holds a kernel of known traffic to scale by")
@@ -316,6 +318,10 @@ def main():
           "gemm_ms": g6_ms, "gemm_tflops": float(flops[0]) / (g6_ms * 1e-3) / 1e12}
     del xc6
 
+    adaln = None
+    if args.adaln_steps > 0:
+        adaln = adaln_sweep(oq, workloads, dev, args.adaln_steps)
+
     trunk = None
     if args.trunk_steps > 0:
         trunk = trunk_sweep(oq, workloads, dev, args.trunk_steps)
@@ -370,6 +376,7 @@ def main():
         "fused_epilogue": fused,
         "w4a6": a6,
         "trunk_c5": trunk,
+        "adaln_int4": adaln,
         "cpu_baseline": cpu,
         "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0),
                 "arch": torch.cuda.get_device_properties(0).gcnArchName,
@@ -454,6 +461,80 @@ def trunk_sweep(oq, workloads, dev, steps, warmup=1):
             "quant_frac_of_hbm": qbytes / (q_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "weight_pass_ms": wp_ms, "weight_pass_gbs": wp_bytes / (wp_ms * 1e-3) / 1e9,
             "weights": n_weights, "weight_code_bytes": int(sum(c.numel() for c in wcodes))}
+
+
+def adaln_sweep(oq, workloads, dev, steps, warmup=2):
+    """The adjacent layer type: every AdaLN modulation projection of a FLUX-shaped image DiT at INT4
+    weight round-to-nearest (group 64), one BF16 conditioning token.  Timed two ways per step:
+    the 76 projections one call each, and as one call over their concatenated weight rows (all
+    of them read the same conditioning vector).  Each way is captured in a graph (the launches
+    are a few microseconds long) and every replay is checked against the eager result.  The
+    offline pass over all 3.2e9 weights is timed launch by launch, generation outside."""
+    K = workloads.ADALN_K
+    sizes = [N for N, count in workloads.ADALN_LAYERS for _ in range(count)]
+    Ntot = sum(sizes)
+    q = torch.empty((Ntot, K // 2), dtype=torch.uint8, device=dev)
+    sc = torch.empty((Ntot, K // 64), dtype=torch.float16, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wp_ms, row = 0.0, 0
+    for i, N in enumerate(sizes):
+        W = workloads.adaln_weights(N, i, device=dev)
+        torch.cuda.synchronize()
+        e0.record()
+        oq.adaln_int4_quantize_weights(W, q[row:row + N], sc[row:row + N])
+        e1.record()
+        torch.cuda.synchronize()
+        wp_ms += e0.elapsed_time(e1)
+        row += N
+        del W
+    X = workloads.adaln_tokens(1, device=dev)
+    Y_each = torch.empty((1, Ntot), device=dev)
+    Y_all = torch.empty((1, Ntot), device=dev)
+    offs = np.cumsum([0] + sizes)
+
+    def each():
+        for i in range(len(sizes)):
+            a, b = int(offs[i]), int(offs[i + 1])
+            oq.adaln_int4_linear(X, q[a:b], sc[a:b], out=Y_each[:, a:b])
+
+    def batched():
+        oq.adaln_int4_linear(X, q, sc, out=Y_all)
+
+    out = {"layers": len(sizes), "K": K, "M": 1, "weights": Ntot * K,
+           "weight_bytes": Ntot * (K // 2 + 2 * (K // 64)), "weight_pass_ms": wp_ms,
+           "weight_pass_gbs": Ntot * (2 * K + K // 2 + 2 * (K // 64)) / (wp_ms * 1e-3) / 1e9}
+    for name, fn, Y in (("per_layer", each, Y_each), ("batched", batched, Y_all)):
+        fn()
+        torch.cuda.synchronize()
+        ref = Y.clone()
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            fn()
+        ok = True
+        for _ in range(warmup):
+            Y.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            ok = ok and bool(torch.equal(Y, ref))
+        e0.record()
+        for _ in range(steps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        ok = ok and bool(torch.equal(Y, ref))
+        gbs = out["weight_bytes"] / (ms * 1e-3) / 1e9
+        out[name] = {"ms": ms, "gbs": gbs, "frac_of_hbm": gbs / HBM_PEAK_GBS, "replays_match_eager": ok}
+    out["batched_equals_per_layer"] = bool(torch.equal(Y_all, Y_each))
+    del q, sc
+    return out
 
 
 def cpu_baseline(layers, rows):
