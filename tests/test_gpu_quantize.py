@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2607_02461_amd as oq
 from paper_2607_02461_amd import workloads
-from tests.gpu_util import compare_quantizer, quantize_gpu, log_stats
+from tests.gpu_util import compare_quantizer, quantize_gpu, log_stats, to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -200,3 +200,35 @@ def test_zero_row_count_is_noop():
     X = torch.empty((0, 256), dtype=torch.bfloat16, device=DEV)
     codes, norms = quantize_gpu(X, 4)
     assert codes.shape == (0, 128) and norms.shape == (0,)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4, 6])
+def test_sign_symmetry(bits):
+    # the codebook is antisymmetric and RPBH linear: code(-x) = 2^b - 1 - code(x) off near-ties,
+    # the same norm
+    X = _randn_bf16(65, 3072, seed=21)
+    c_pos, n_pos = quantize_gpu(X, bits)
+    c_neg, n_neg = quantize_gpu(-X, bits)
+    gp = oracle.unpack_codes(c_pos.cpu().numpy(), bits, 3072)
+    gn = oracle.unpack_codes(c_neg.cpu().numpy(), bits, 3072)
+    ocb = oracle.lloydmax_codebook(bits, 3072)
+    _, _, U = oracle.quantize_act(to_f64(X), oracle.rpbh_plan(3072, 128, 0), ocb)
+    near = oracle.near_tie_mask(U, ocb.thresholds, 1e-5)
+    bad = int(np.sum((gn != (1 << bits) - 1 - gp) & ~near))
+    log_stats(f"sign symmetry b={bits}", near_ties=int(near.sum()), mismatches_off_tie=bad)
+    assert bad == 0
+    assert torch.equal(n_pos, n_neg)
+
+
+def test_zero_row_gives_zero_output_row():
+    K, N = 1024, 300
+    X = _randn_bf16(5, K, seed=31)
+    X[3] = 0
+    W = _randn_bf16(N, K, seed=32, scale=0.02)
+    plan = oq.rpbh_plan(K, 128, 0)
+    cb = oq.lloydmax_codebook(4, K)
+    wc, wn = oq.quantize_weights_offline(plan, cb, W)
+    xc, xn = oq.rpbh_quantize_act(plan, cb, X)
+    Y = oq.orbit_qlinear(cb, xc, xn, cb, wc, wn)
+    torch.cuda.synchronize()
+    assert torch.all(Y[3] == 0) and torch.all(Y[[0, 1, 2, 4]].abs().sum(dim=1) > 0)

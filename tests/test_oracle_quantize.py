@@ -187,3 +187,13 @@ def test_layer_epilogue_closed_forms():
     assert abs(oracle.layer_epilogue(Y, bias=b, gelu=True)[0, 0] - 0.5 * 0.6914624612740131) < 1e-15
     r = oracle.layer_epilogue(np.array([[1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 1.0 + 2 ** -9]]), out_bf16=True)
     assert r[0, 0] == 1.0 and r[0, 1] == 1.0 + 2 ** -6 and r[0, 2] == 1.0   # half-ulp ties go to even
+
+
+def test_row_norm_storage_overhead():
+    # Sec. 4.2: the bf16 norm r' costs 16 bits per row against b_w * d bits of codes, under 0.3%
+    # for every evaluated width and bit-width
+    for d in (3072, 5120, 12288, 13824):
+        for bw in (2, 3, 4):
+            code_bytes = oracle.pack_codes(np.zeros((1, d), dtype=np.int64), bw).shape[1]
+            assert code_bytes == d * bw // 8
+            assert 2 / code_bytes < 0.003
