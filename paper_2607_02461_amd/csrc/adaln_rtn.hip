@@ -14,9 +14,9 @@
 // weights once, so it is bound by HBM and, a few microseconds long per projection, by how much
 // of it is in flight: groups of 16 lanes own two output rows, each lane issues the loads of up
 // to four 32-code chunks per row before computing, and the activations sit in LDS, staged once
-// by each persistent workgroup.  A code
-// nibble u becomes the BF16 value 128 + u by OR-ing it into the mantissa of 128 (0x4300 | u is exact: 128..143 are BF16 integers), two per register
-// at bits 0 and 16, so one v_dot2_f32_bf16 takes two codes against two activations with exact
+// by each persistent workgroup.  A code nibble u becomes the BF16 value 128 + u by OR-ing it into
+// the mantissa of 128 (0x4300 | u is exact: 128..143 are BF16 integers), two per register at
+// bits 0 and 16, so one v_dot2_f32_bf16 takes two codes against two activations with exact
 // products; per chunk the accumulator starts at -136 * sum(x), which removes the 128 + 8 offset.
 // The activations of a chunk are paired to match: element j of each 8 with element j + 4.
 #include <hip/hip_runtime.h>

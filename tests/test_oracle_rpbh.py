@@ -167,3 +167,64 @@ def test_permutation_spreads_a_clustered_outlier():
     assert max(mass) < 0.2
     z_id = oracle.rpbh_forward(x[None, :], ident)[0]
     assert np.max(np.abs(z_id[h:])) < 1e-2       # blocks 1.. saw no outlier energy
+
+
+def _violations(values, bound):
+    return int(np.sum(np.asarray(values) > bound))
+
+
+def test_lemma1_per_block_incoherence():
+    # Suppl. proof sketch, Lemma 1: for any partition, over the signs, ||z||_inf <= sqrt(2 log(4d/delta)/h)
+    # with probability >= 1 - delta/2.  The test vector is the worst case for a missing sign: a flat
+    # block holding all the mass (without D, H maps it to a single spike of size 1)
+    d, h, delta, trials = 3072, 128, 0.05, 300
+    x = np.zeros(d)
+    x[:h] = 1.0 / np.sqrt(h)
+    bound = math.sqrt(2 * math.log(4 * d / delta) / h)
+    rng = np.random.default_rng(11)
+    norms = []
+    for _ in range(trials):
+        p = oracle.Plan(d=d, h=h, perm=np.arange(d), sign=rng.choice([-1.0, 1.0], size=d))
+        norms.append(np.max(np.abs(oracle.rpbh_forward(x[None, :], p))))
+    assert _violations(norms, bound) <= delta / 2 * trials
+    no_sign = oracle.Plan(d=d, h=h, perm=np.arange(d), sign=np.ones(d))
+    assert np.max(np.abs(oracle.rpbh_forward(x[None, :], no_sign))) > 0.99 > bound
+
+
+def test_lemma2_mass_balancing():
+    # Lemma 2: over pi, |M_j - 1/k| <= mu_inf sqrt((h/2) log(4k/delta)) for all j, w.p. >= 1 - delta/2
+    d, h, delta, trials = 3072, 128, 0.05, 300
+    k = d // h
+    rng = np.random.default_rng(12)
+    x = 1.0 + 0.1 * rng.random(d)
+    x[:h] *= 1.5                                    # block 0 of the channels is heavier
+    x /= np.linalg.norm(x)
+    mu = np.max(x * x)
+    bound = mu * math.sqrt(h / 2 * math.log(4 * k / delta))
+    devs = []
+    for t in range(trials):
+        p = oracle.rpbh_plan(d, h, seed=1000 + t)
+        y = x[p.perm]
+        M = np.sum(y.reshape(k, h) ** 2, axis=1)
+        devs.append(np.max(np.abs(M - 1.0 / k)))
+    assert _violations(devs, bound) <= delta / 2 * trials
+    # without pi the heavier channels stay together in block 0, beyond the bound
+    M0 = np.sum(x[:h] ** 2)
+    assert abs(M0 - 1.0 / k) > bound
+
+
+def test_proposition_sup_norm_bound():
+    # Proposition (restated in the supplement): ||Pi_d x||_inf <= sqrt((2/d)(1 + rho) log(4d/delta)),
+    # rho = d mu_inf sqrt(log(4k/delta) / (2h)), w.p. >= 1 - delta over the plan
+    d, h, delta, trials = 3072, 128, 0.05, 200
+    k = d // h
+    rng = np.random.default_rng(13)
+    x = rng.standard_normal(d)
+    x /= np.linalg.norm(x)
+    mu = np.max(x * x)
+    rho = d * mu * math.sqrt(math.log(4 * k / delta) / (2 * h))
+    bound = math.sqrt(2.0 / d * (1 + rho) * math.log(4 * d / delta))
+    norms = [np.max(np.abs(oracle.rpbh_forward(x[None, :], oracle.rpbh_plan(d, h, seed=2000 + t))))
+             for t in range(trials)]
+    assert _violations(norms, bound) <= delta * trials
+    assert max(norms) > 0.3 * bound                 # the bound is not vacuous at this size
