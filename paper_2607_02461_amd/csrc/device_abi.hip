@@ -266,7 +266,9 @@ orbit_status adaln_int4_quantize_weights(const uint16_t* W, int64_t N, int64_t K
     if (N < 0) return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: negative N");
     if (K <= 0 || K % 64 != 0) return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: K=%lld must be a positive multiple of 64", (long long)K);
     if (ldw < K || ldw % 8 != 0) return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: ldw=%lld must be >= K and a multiple of 8", (long long)ldw);
-    if (K > (int64_t)1 << 30 || N > INT32_MAX) return fail(ORBIT_EUNSUPPORTED, "adaln_int4_quantize_weights: N or K too large");
+    // one thread per group of 64: the launch grid is 32-bit
+    if (K > (int64_t)1 << 30 || N > INT32_MAX || N * (K / 64) > (int64_t)INT32_MAX * 256)
+        return fail(ORBIT_EUNSUPPORTED, "adaln_int4_quantize_weights: N or K too large");
     if (N == 0) return ORBIT_OK;
     if (!W || !q || !scales) return fail(ORBIT_EINVAL, "adaln_int4_quantize_weights: null device pointer");
     if (!aligned(W, 16) || !aligned(q, 16) || !aligned(scales, 2))

@@ -227,6 +227,10 @@ def test_adaln_calls_validate_before_launch():
         (lib.adaln_int4_linear, (fake, 2, 128, null, fake, 16, 128, null, fake, 16, null), oq.ORBIT_EINVAL),
         (lib.adaln_int4_linear, (fake, 1 << 20, 128, fake, fake, 16, 128, null, fake, 16, null),
          oq.ORBIT_EUNSUPPORTED),
+        (lib.adaln_int4_linear, (fake, 2, 32768, fake, fake, 16, 32768, null, fake, 16, null),
+         oq.ORBIT_EUNSUPPORTED),                                                                      # K > 16384
+        (lib.adaln_int4_quantize_weights, (fake, 1 << 30, 1 << 20, 1 << 20, fake, fake, null),
+         oq.ORBIT_EUNSUPPORTED),                                                                      # grid > 2^31
     ]
     for fn, args, want in cases:
         st, msg = _status(fn, *args)
