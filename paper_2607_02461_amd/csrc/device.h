@@ -44,7 +44,9 @@ struct QuantParams {
 
 int quant_rows_per_group(int K);
 size_t quant_smem_bytes(int K, int R, int ncell);
-hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, int grid, hipStream_t stream);
+// gather: apply the permutation through the LDS-staged gather (false only for the identity)
+hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, bool gather, int grid,
+                                hipStream_t stream);
 
 // LUT-decode GEMM: Y = diag(sx) La[Xc] (Lw[Wc])^T diag(rw).
 struct GemmParams {

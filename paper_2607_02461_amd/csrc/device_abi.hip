@@ -153,7 +153,7 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     q.sqrt_h = (float)std::sqrt((double)p->h);
     // two workgroups fit a compute unit (LDS: row buffer + encoder table + block partials)
     const int grid = (int)std::min<int64_t>(q.ngroups, (int64_t)info.cus * 2);
-    hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, grid, (hipStream_t)stream);
+    hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, !p->identity, grid, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, who);
     return ORBIT_OK;
 }

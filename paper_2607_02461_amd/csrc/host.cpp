@@ -337,6 +337,8 @@ orbit_status rpbh_plan_from_arrays(int64_t d, int32_t h, const int32_t* perm, co
     }
     p->d = d;
     p->h = h;
+    p->identity = true;
+    for (int64_t j = 0; j < d && p->identity; ++j) p->identity = p->perm[j] == j;
     *out = p;
     return ORBIT_OK;
 }

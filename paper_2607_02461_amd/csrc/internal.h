@@ -25,6 +25,7 @@ struct orbit_plan_s {
     int32_t h = 0;
     std::vector<int32_t> perm;  // y_j = x[perm[j]]
     std::vector<int8_t> sign;   // multiplies post-permutation coordinate j
+    bool identity = false;      // perm[j] == j for every j (Block-RHT, full-dimension rotations)
     // Per-device tables for the quantizer (gather offsets and sign masks), see plan_meta().
     std::mutex mu;
     uint32_t* dev_meta[orbit::kMaxDevices] = {};

@@ -132,13 +132,36 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
 }
 
-// First butterfly stage from a bf16 pair (y0, y1): y0 + y1 and y0 - y1 as the three-operand
-// v_dot2_f32_bf16 against (1, 1) held in an SGPR, with neg_hi giving (1, -1).  (The accumulating
-// two-operand form the compiler picks would need its destination zeroed first.)
-__device__ __forceinline__ void stage1(uint32_t P, uint32_t one_one, float& sum, float& diff) {
-    asm("v_dot2_f32_bf16 %0, %1, %2, 0" : "=v"(sum) : "v"(P), "s"(one_one));
-    asm("v_dot2_f32_bf16 %0, %1, %2, 0 neg_hi:[0,1,0]" : "=v"(diff) : "v"(P), "s"(one_one));
-}
+// First butterfly stage of eight bf16 pairs (y0, y1) = P[B .. B+7]: y0 + y1 and y0 - y1 as the
+// three-operand v_dot2_f32_bf16 against (1, 1) held in an SGPR, with neg_hi giving (1, -1), into
+// Z[2B .. 2B+15].  (The accumulating two-operand form the compiler picks would need its destination
+// zeroed first.)  A DOT result needs wait states before another VALU op may read it, and the
+// compiler's hazard tracking does not look inside asm, so the block ends with an s_nop covering
+// them; the outputs are early-clobber because the block writes some before it reads the rest.
+#define ORBIT_STAGE1_8(Z, P, B, ONE)                                                               \
+    asm("v_dot2_f32_bf16 %0, %16, %24, 0\n"                                                        \
+        "v_dot2_f32_bf16 %1, %16, %24, 0 neg_hi:[0,1,0]\n"                                         \
+        "v_dot2_f32_bf16 %2, %17, %24, 0\n"                                                        \
+        "v_dot2_f32_bf16 %3, %17, %24, 0 neg_hi:[0,1,0]\n"                                         \
+        "v_dot2_f32_bf16 %4, %18, %24, 0\n"                                                        \
+        "v_dot2_f32_bf16 %5, %18, %24, 0 neg_hi:[0,1,0]\n"                                         \
+        "v_dot2_f32_bf16 %6, %19, %24, 0\n"                                                        \
+        "v_dot2_f32_bf16 %7, %19, %24, 0 neg_hi:[0,1,0]\n"                                         \
+        "v_dot2_f32_bf16 %8, %20, %24, 0\n"                                                        \
+        "v_dot2_f32_bf16 %9, %20, %24, 0 neg_hi:[0,1,0]\n"                                         \
+        "v_dot2_f32_bf16 %10, %21, %24, 0\n"                                                       \
+        "v_dot2_f32_bf16 %11, %21, %24, 0 neg_hi:[0,1,0]\n"                                        \
+        "v_dot2_f32_bf16 %12, %22, %24, 0\n"                                                       \
+        "v_dot2_f32_bf16 %13, %22, %24, 0 neg_hi:[0,1,0]\n"                                        \
+        "v_dot2_f32_bf16 %14, %23, %24, 0\n"                                                       \
+        "v_dot2_f32_bf16 %15, %23, %24, 0 neg_hi:[0,1,0]\n"                                        \
+        "s_nop 4"                                                                                  \
+        : "=&v"(Z[2 * B + 0]), "=&v"(Z[2 * B + 1]), "=&v"(Z[2 * B + 2]), "=&v"(Z[2 * B + 3]),      \
+          "=&v"(Z[2 * B + 4]), "=&v"(Z[2 * B + 5]), "=&v"(Z[2 * B + 6]), "=&v"(Z[2 * B + 7]),      \
+          "=&v"(Z[2 * B + 8]), "=&v"(Z[2 * B + 9]), "=&v"(Z[2 * B + 10]), "=&v"(Z[2 * B + 11]),    \
+          "=&v"(Z[2 * B + 12]), "=&v"(Z[2 * B + 13]), "=&v"(Z[2 * B + 14]), "=&v"(Z[2 * B + 15])   \
+        : "v"(P[B + 0]), "v"(P[B + 1]), "v"(P[B + 2]), "v"(P[B + 3]), "v"(P[B + 4]),               \
+          "v"(P[B + 5]), "v"(P[B + 6]), "v"(P[B + 7]), "s"(ONE))
 
 template <int BITS>
 __device__ __forceinline__ void store_packed(uint8_t* dst, const uint32_t (&w)[6]) {
@@ -245,13 +268,15 @@ __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[6
     }
 }
 
-template <int BITS, bool NORM_BF16, bool OUTER>
+template <int BITS, bool NORM_BF16, bool OUTER, bool GATHER>
 struct Quantizer {
     const QuantParams& p;
     unsigned char* smem;
     int tid, T, q, rg, blk;
     bool active;         // lane owns a (row slot, block) of the group
-    uint32_t addr[32];   // byte offset of each gathered element inside the staged group
+    uint32_t addr[32];   // staged gather: byte offset of each gathered element inside the staged group
+    uint32_t mask[16];   // direct loads: bf16 sign bits of this lane's 16 element pairs
+    uint32_t xoff;       // direct loads: byte offset of this lane's 64 bytes from the group's first row
     float sigma;
     float sgn1, sgn2, sgn3, sgn4;  // +1 / -1: lower / upper partner in the in-row butterfly stages
     int chunk;           // position (in 32-code units) of this lane's outputs in the row
@@ -289,37 +314,62 @@ struct Quantizer {
         }
     }
 
+    // Identity permutation: the 32 positions a lane transforms are 64 consecutive bytes of its row,
+    // read straight into registers (lanes without a block of a valid row keep what they hold).
+    __device__ __forceinline__ void load_direct(int g, u32x4 (&v)[4]) const {
+        const char* base = (const char*)p.X + (int64_t)g * p.R * p.ldx * 2;
+        uint32_t off = xoff;
+        asm volatile("" : "+v"(off));
+        if (active && rg < rows_of(g)) {
+            const u32x4* src = (const u32x4*)(base + off);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = __builtin_nontemporal_load(src + k);
+        }
+    }
+
     // One row group.  Every lane runs the arithmetic (lanes without a block of a valid row work on
-    // harmless LDS data); only the stores are guarded, so the hot path has no divergence.
-    __device__ __forceinline__ void iteration(int g) {
+    // harmless data); only the stores are guarded, so the hot path has no divergence.  `pf` carries
+    // the direct loads of this group in and those of the next group out; `it` counts iterations.
+    __device__ __forceinline__ void iteration(int g, int it, u32x4 (&pf)[4]) {
         const int next = g + gridDim.x;
         const int nb = p.nb;
         const int nrows = rows_of(g);
         const int64_t row0 = (int64_t)g * p.R;
         const bool owner = active && rg < nrows;
-        float* part = (float*)(smem + kEncOff + p.ncell * 4);
+        // Block partials.  With direct loads the iteration has a single barrier, so the partials
+        // alternate between two buffers: a wave writes the next group's partials only after the
+        // barrier that every wave passes once it has finished reading this group's.
+        float* part = (float*)(smem + kEncOff + p.ncell * 4) + (GATHER ? 0 : (it & 1) * p.R * nb);
 
-        // gathered pairs: element 2i in the low half, 2i+1 in the high half of P[i]
-        // (built as a two-lane vector, the pair becomes one v_perm of the two loads with no
-        // masking of the zero-extended halves)
+        // element pairs: element 2i in the low half, 2i+1 in the high half of P[i]
         uint32_t P[16];
+        if constexpr (GATHER) {
+            // (built as a two-lane vector, the pair becomes one v_perm of the two loads with no
+            // masking of the zero-extended halves)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            u16x2 v;
-            v.x = *(const uint16_t*)(smem + addr[2 * i]);
-            v.y = *(const uint16_t*)(smem + addr[2 * i + 1]);
-            P[i] = __builtin_bit_cast(uint32_t, v);
+            for (int i = 0; i < 16; ++i) {
+                u16x2 v;
+                v.x = *(const uint16_t*)(smem + addr[2 * i]);
+                v.y = *(const uint16_t*)(smem + addr[2 * i + 1]);
+                P[i] = __builtin_bit_cast(uint32_t, v);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) P[i] = pf[i >> 2][i & 3] ^ mask[i];
         }
-        u32x4 pf[4];
-        if (next < p.ngroups) load_group(next, pf);
+        if (next < p.ngroups) {
+            if constexpr (GATHER)
+                load_group(next, pf);
+            else
+                load_direct(next, pf);
+        }
 
         float z[32];
         float ss = 0.f;
+        ORBIT_STAGE1_8(z, P, 0, p.one_one);
+        ORBIT_STAGE1_8(z, P, 8, p.one_one);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            stage1(P[i], p.one_one, z[2 * i], z[2 * i + 1]);
-            ss = dot2(P[i], P[i], ss);
-        }
+        for (int i = 0; i < 16; ++i) ss = dot2(P[i], P[i], ss);
 #pragma unroll
         for (int s = 2; s < 32; s <<= 1) {
 #pragma unroll
@@ -423,17 +473,21 @@ struct Quantizer {
         pack_codes<BITS>(y, w);
         if (owner)
             store_packed<BITS>(p.codes + (row0 + rg) * ((int64_t)p.K * BITS / 8) + (int64_t)(OUTER ? chunk : blk * 4 + q) * 4 * BITS, w);
-        if (next < p.ngroups) {
-            store_group(next, pf);
-            __syncthreads();
+        if constexpr (GATHER) {
+            if (next < p.ngroups) {
+                store_group(next, pf);
+                __syncthreads();
+            }
         }
     }
 };
 
-template <int BITS, bool NORM_BF16, bool OUTER>
+// GATHER: the permutation is applied by staging each row group in LDS and gathering from it; without
+// it (identity permutation: Block-RHT and full-dimension rotations) lanes load their data directly.
+template <int BITS, bool NORM_BF16, bool OUTER, bool GATHER>
 __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
-    Quantizer<BITS, NORM_BF16, OUTER> Q{p, smem};
+    Quantizer<BITS, NORM_BF16, OUTER, GATHER> Q{p, smem};
     Q.tid = threadIdx.x;
     Q.T = blockDim.x;
     const int task = Q.tid >> 2;
@@ -473,17 +527,17 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
                 if ((task >> j) & 1) Q.sigma = -Q.sigma;
         }
     }
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int c = Q.tid + k * Q.T, r = c / Q.cpr;
-        Q.goff[k] = (uint32_t)(r * p.ldx * 2 + (c - r * Q.cpr) * 16);
-    }
-
     // encoder table -> LDS
     float* tab = (float*)(smem + kEncOff);
     for (int i = Q.tid; i < p.ncell; i += Q.T) tab[i] = p.enc[i];
 
-    {
+    u32x4 pf[4] = {};
+    if constexpr (GATHER) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int c = Q.tid + k * Q.T, r = c / Q.cpr;
+            Q.goff[k] = (uint32_t)(r * p.ldx * 2 + (c - r * Q.cpr) * 16);
+        }
         const uint4* src = (const uint4*)(p.meta + Q.blk * 128 + Q.q * 32);
         const uint32_t rowoff = (uint32_t)(Q.rg * p.K * 2);
 #pragma unroll
@@ -493,28 +547,42 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) Q.addr[4 * i + k] = Q.active ? rowoff + m[k] : 0u;
         }
-    }
-
-    if (blockIdx.x < p.ngroups) {
-        u32x4 pf[4];
-        Q.load_group(blockIdx.x, pf);
-        Q.store_group(blockIdx.x, pf);
+        if (blockIdx.x < p.ngroups) {
+            Q.load_group(blockIdx.x, pf);
+            Q.store_group(blockIdx.x, pf);
+        }
+    } else {
+        // with the identity permutation the sign mask of source pair i is that of position pair i
+        const int pos = Q.active ? Q.blk * 128 + Q.q * 32 : 0;
+        const uint4* src = (const uint4*)(p.smask + pos / 2);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint4 v = src[i];
+            Q.mask[4 * i] = v.x;
+            Q.mask[4 * i + 1] = v.y;
+            Q.mask[4 * i + 2] = v.z;
+            Q.mask[4 * i + 3] = v.w;
+        }
+        Q.xoff = (uint32_t)(Q.rg * p.ldx * 2 + pos * 2);
+        if (blockIdx.x < p.ngroups) Q.load_direct(blockIdx.x, pf);
     }
     __syncthreads();
-    for (int g = blockIdx.x; g < p.ngroups; g += gridDim.x) Q.iteration(g);
+    int it = 0;
+    for (int g = blockIdx.x; g < p.ngroups; g += gridDim.x) Q.iteration(g, it++, pf);
 }
 
-template <int BITS, bool NB, bool OUTER>
+template <int BITS, bool NB, bool OUTER, bool GATHER>
 hipError_t set_smem_limit() {
     static std::atomic<uint64_t> done{0};
-    return raise_lds_limit((const void*)rpbh_quantize_kernel<BITS, NB, OUTER>, 160 * 1024, done);
+    return raise_lds_limit((const void*)rpbh_quantize_kernel<BITS, NB, OUTER, GATHER>, 160 * 1024, done);
 }
 
 }  // namespace
 
 size_t quant_smem_bytes(int K, int R, int ncell) {
     const int nb = K / 128;
-    return (size_t)kEncOff + (size_t)ncell * 4 + (size_t)R * nb * 4 + (size_t)R * 4;
+    // row buffer, encoder table, two sets of block partials (the direct-load path alternates them)
+    return (size_t)kEncOff + (size_t)ncell * 4 + (size_t)R * nb * 8 + (size_t)R * 4;
 }
 
 int quant_rows_per_group(int K) {
@@ -522,29 +590,36 @@ int quant_rows_per_group(int K) {
     return nb >= 128 ? 1 : 128 / nb;
 }
 
-hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, int grid, hipStream_t stream) {
+hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, bool gather, int grid,
+                                hipStream_t stream) {
     const int threads = ((p.R * p.nb * 4 + 63) / 64) * 64;
     const size_t smem = quant_smem_bytes(p.K, p.R, p.ncell);
-#define ORBIT_LAUNCH(B, NB, OU)                                                                    \
+#define ORBIT_LAUNCH(B, NB, OU, GA)                                                                \
     do {                                                                                           \
-        const hipError_t e = set_smem_limit<B, NB, OU>();                                          \
+        const hipError_t e = set_smem_limit<B, NB, OU, GA>();                                      \
         if (e != hipSuccess) return e;                                                             \
-        hipLaunchKernelGGL((rpbh_quantize_kernel<B, NB, OU>), dim3(grid), dim3(threads), smem, stream, p); \
+        hipLaunchKernelGGL((rpbh_quantize_kernel<B, NB, OU, GA>), dim3(grid), dim3(threads), smem, stream, p); \
     } while (0)
-#define ORBIT_LAUNCH_BITS(NB, OU)                                                                  \
+#define ORBIT_LAUNCH_BITS(NB, OU, GA)                                                              \
     do {                                                                                           \
-        if (bits == 2) ORBIT_LAUNCH(2, NB, OU);                                                    \
-        else if (bits == 3) ORBIT_LAUNCH(3, NB, OU);                                               \
-        else if (bits == 6) ORBIT_LAUNCH(6, NB, OU);                                               \
-        else ORBIT_LAUNCH(4, NB, OU);                                                              \
+        if (bits == 2) ORBIT_LAUNCH(2, NB, OU, GA);                                                \
+        else if (bits == 3) ORBIT_LAUNCH(3, NB, OU, GA);                                           \
+        else if (bits == 6) ORBIT_LAUNCH(6, NB, OU, GA);                                           \
+        else ORBIT_LAUNCH(4, NB, OU, GA);                                                          \
+    } while (0)
+#define ORBIT_LAUNCH_OUTER(NB, GA)                                                                 \
+    do {                                                                                           \
+        if (p.outer > 0) ORBIT_LAUNCH_BITS(NB, true, GA);                                          \
+        else ORBIT_LAUNCH_BITS(NB, false, GA);                                                     \
     } while (0)
     if (norm_bf16) {
-        if (p.outer > 0) ORBIT_LAUNCH_BITS(true, true);
-        else ORBIT_LAUNCH_BITS(true, false);
+        if (gather) ORBIT_LAUNCH_OUTER(true, true);
+        else ORBIT_LAUNCH_OUTER(true, false);
     } else {
-        if (p.outer > 0) ORBIT_LAUNCH_BITS(false, true);
-        else ORBIT_LAUNCH_BITS(false, false);
+        if (gather) ORBIT_LAUNCH_OUTER(false, true);
+        else ORBIT_LAUNCH_OUTER(false, false);
     }
+#undef ORBIT_LAUNCH_OUTER
 #undef ORBIT_LAUNCH_BITS
 #undef ORBIT_LAUNCH
     return hipGetLastError();

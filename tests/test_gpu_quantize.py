@@ -177,8 +177,8 @@ def test_plan_from_caller_arrays():
 
 @pytest.mark.parametrize("K,h", [(3072, 128), (3072, 1024), (4096, 4096)])
 def test_rotation_classes_without_permutation(K, h):
-    # Block-RHT (RPBH without the permutation) and, for h = K = 4096, Full RHT: the same kernel
-    # with an identity gather (the rotation classes of the paper's ablation, Table 4)
+    # Block-RHT (RPBH without the permutation) and, for h = K = 4096, Full RHT (the rotation
+    # classes of the paper's ablation, Table 4)
     signs = oq.rpbh_plan(K, h, 0).arrays()[1]
     ident = np.arange(K)
     plan = oq.rpbh_plan_from_arrays(K, h, ident, signs)
@@ -187,6 +187,57 @@ def test_rotation_classes_without_permutation(K, h):
     X[:, 5:37] = X[:, 5:37] * 30          # clustered outlier channels
     for bits in (2, 4):
         compare_quantizer(f"rotation class identity-pi K={K} h={h}", X, bits, plan=plan, oplan=oplan)
+
+
+def _identity_plans(K, h, seed=0):
+    signs = oq.rpbh_plan(K, h, seed).arrays()[1]
+    ident = np.arange(K)
+    return (oq.rpbh_plan_from_arrays(K, h, ident, signs),
+            oracle.Plan(d=K, h=h, perm=ident.astype(np.int64), sign=signs.astype(np.float64)))
+
+
+# An identity permutation takes the kernel's direct-load path (each lane reads its 32 consecutive
+# elements straight from HBM, no LDS staging): every block size, bit width and norm type, with
+# ragged row counts.
+@pytest.mark.parametrize("K,h,M", [(128, 128, 3), (1024, 128, 131), (2560, 256, 50), (1536, 512, 40),
+                                   (5120, 1024, 30), (6144, 2048, 11), (8192, 4096, 6), (16384, 4096, 3),
+                                   (13824, 512, 5), (16384, 128, 2)])
+@pytest.mark.parametrize("weights", [False, True])
+def test_identity_permutation_direct_loads(K, h, M, weights):
+    plan, oplan = _identity_plans(K, h, seed=K % 7)
+    X = _randn_bf16(M, K, seed=K + 3 * h + M)
+    for bits in (4,) if weights else (2, 3, 4, 6):
+        compare_quantizer(f"identity-pi K={K} h={h} M={M}", X, bits, weights=weights, plan=plan, oplan=oplan)
+
+
+def test_identity_permutation_many_group_iterations():
+    # enough row groups (64 rows each at K = 256) that every persistent workgroup runs several
+    # iterations, alternating its two buffers of block partials; every row checked
+    K, M = 256, 100003
+    plan, oplan = _identity_plans(K, 128, seed=3)
+    X = _randn_bf16(M, K, seed=17)
+    compare_quantizer("identity-pi many iterations", X, 4, plan=plan, oplan=oplan)
+    plan2, oplan2 = _identity_plans(K, 256, seed=4)
+    compare_quantizer("identity-pi many iterations h=256", X, 3, weights=True, plan=plan2, oplan=oplan2)
+
+
+def test_identity_permutation_strided_rows():
+    base = _randn_bf16(41, 3072 + 64, seed=12)
+    X = base[:, 32:32 + 3072]            # ldx = 3136, rows start 64 bytes in
+    plan, oplan = _identity_plans(3072, 1024, seed=2)
+    compare_quantizer("identity-pi strided rows", X, 4, plan=plan, oplan=oplan)
+
+
+def test_c4_up_block_rht_sampled_rows():
+    # Block-RHT on the full up-projection input, in the launch configuration the benchmark's
+    # rotation-class comparison times (h = 128 and the paper's rule, h = 1024)
+    fr, tpf, txt = 21, 30 * 52, 512
+    X = workloads.video_acts(fr * tpf, txt, 5120, 4, fr, workloads.C4.data_seed, 0, device=DEV)
+    rows = np.sort(np.random.default_rng(49).choice(X.shape[0], 2048, replace=False))
+    rows[-1] = X.shape[0] - 1
+    for h in (128, 1024):
+        plan, oplan = _identity_plans(5120, h, seed=0)
+        compare_quantizer(f"c4 up act sampled, Block-RHT h={h}", X, 4, rows=rows, plan=plan, oplan=oplan)
 
 
 def test_strided_rows():
