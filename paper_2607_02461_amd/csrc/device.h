@@ -26,8 +26,9 @@ struct QuantParams {
     const uint16_t* X;     // bf16 [M][ldx]
     int64_t ldx;           // elements
     int64_t M;
-    const uint32_t* meta;  // [K]: 2*perm[j], the byte offset of the gathered element in a staged row
-    const uint32_t* smask; // [K/2]: bf16 sign bits to XOR into staged element pairs (source positions)
+    const uint32_t* meta;  // [K]: 2*perm[j], the byte offset of the gathered element in a staged row,
+                           // with bit 31 set where sign[j] = -1
+    const uint32_t* smask; // [K/2]: bf16 sign bits of position pairs (the identity-permutation path)
     uint8_t* codes;        // [M][K*bits/8]
     void* norm;            // fp32 or bf16 [M]
     int K, nb, R;          // input dim, K/128 blocks, rows staged per workgroup iteration
@@ -40,13 +41,19 @@ struct QuantParams {
     uint32_t one_one;      // bf16 pair (1.0, 1.0), 0x3F803F80
     int outer;             // log2(h / 128): Hadamard stages across 128-blocks (0 for h = 128)
     float sqrt_h;          // sqrt(h), the FWHT's normalization
+    // staging: the row of 16-byte chunk c of a group is (c * row_magic) >> row_shift (exact for
+    // every chunk a workgroup stages), and the chunk sits row_gap = 2*(ldx - K) bytes per row
+    // further than in a contiguous group
+    uint32_t row_magic, row_shift, row_gap;
+    // LDS layout in bytes (set by the launcher): encoder table at 0, block partials at part_off,
+    // staged rows at row_off and their negated copy neg_off bytes further
+    uint32_t part_off, row_off, neg_off;
 };
 
 int quant_rows_per_group(int K);
-size_t quant_smem_bytes(int K, int R, int ncell);
-// gather: apply the permutation through the LDS-staged gather (false only for the identity)
-hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, bool gather, int grid,
-                                hipStream_t stream);
+// gather: apply the permutation through the LDS-staged gather (false only for the identity).
+// Launches a persistent grid of at most two workgroups per compute unit.
+hipError_t launch_rpbh_quantize(QuantParams p, int bits, bool norm_bf16, bool gather, int cus, hipStream_t stream);
 
 // LUT-decode GEMM: Y = diag(sx) La[Xc] (Lw[Wc])^T diag(rw).
 struct GemmParams {

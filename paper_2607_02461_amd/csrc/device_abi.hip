@@ -45,22 +45,18 @@ orbit_status current_device(int* dev, DeviceInfo* info) {
 }
 
 // The plan's tables on device `dev`, uploaded on first use: K gather offsets (2*perm[j], the
-// byte offset of the element that moves to position j) followed by K/2 sign masks over source
-// positions (bit 15 / bit 31 of word i carry the sign applied to source elements 2i / 2i+1, i.e.
-// the sign of the position each of them moves to), repeated once per row slot of a staged group.
+// byte offset of the element that moves to position j, with bit 31 set where sign[j] = -1)
+// followed by K/2 sign masks over positions (bit 15 / bit 31 of word i carry sign[2i] /
+// sign[2i+1]), which the identity-permutation path applies to the pairs it loads.
 orbit_status plan_meta(orbit_plan p, int dev, const uint32_t** out) {
     std::lock_guard<std::mutex> lk(p->mu);
     if (!p->dev_meta[dev]) {
         const int64_t d = p->d;
-        const int64_t reps = d % 2 == 0 && d <= kQuantMaxK ? quant_rows_per_group((int)d) : 1;
-        std::vector<uint32_t> meta((size_t)(d + reps * ((d + 1) / 2)), 0u);
+        std::vector<uint32_t> meta((size_t)(d + (d + 1) / 2), 0u);
         for (int64_t j = 0; j < d; ++j) {
-            const uint32_t src = (uint32_t)p->perm[j];
-            meta[j] = src * 2u;
-            if (p->sign[j] < 0) meta[d + src / 2] |= (src & 1u) ? 0x80000000u : 0x8000u;
+            meta[j] = (uint32_t)p->perm[j] * 2u | (p->sign[j] < 0 ? 0x80000000u : 0u);
+            if (p->sign[j] < 0) meta[d + j / 2] |= (j & 1) ? 0x80000000u : 0x8000u;
         }
-        for (int64_t r = 1; r < reps; ++r)
-            std::memcpy(&meta[d + r * (d / 2)], &meta[d], sizeof(uint32_t) * (d / 2));
         void* dp = nullptr;
         hipError_t e = hipMalloc(&dp, meta.size() * sizeof(uint32_t));
         if (e != hipSuccess) return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "plan upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
@@ -110,7 +106,7 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     if (cb->bits < 2 || cb->bits > 6 || cb->bits == 5)
         return fail(ORBIT_EUNSUPPORTED, "%s: %d-bit codes not implemented (2, 3, 4 and 6 are)", who, cb->bits);
     if (K > kQuantMaxK) return fail(ORBIT_EUNSUPPORTED, "%s: K=%lld above %lld", who, (long long)K, (long long)kQuantMaxK);
-    if ((int64_t)quant_rows_per_group((int)K) * ldx * 2 >= ((int64_t)1 << 31))
+    if ((int64_t)quant_rows_per_group((int)K) * ldx * 2 >= ((int64_t)1 << 31) || (ldx - K) * 2 >= ((int64_t)1 << 24))
         return fail(ORBIT_EUNSUPPORTED, "%s: row stride %lld too large", who, (long long)ldx);
     if (M > INT32_MAX) return fail(ORBIT_EUNSUPPORTED, "%s: M=%lld above 2^31-1 rows", who, (long long)M);
     if (cb->enc.ncell > kQuantMaxCells)
@@ -151,9 +147,25 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     q.outer = 0;
     while ((kQuantH << q.outer) < p->h) ++q.outer;
     q.sqrt_h = (float)std::sqrt((double)p->h);
-    // two workgroups fit a compute unit (LDS: row buffer + encoder table + block partials)
-    const int grid = (int)std::min<int64_t>(q.ngroups, (int64_t)info.cus * 2);
-    hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, !p->identity, grid, (hipStream_t)stream);
+    // row of a staged chunk: an exact multiply-shift division by the chunks per row for every
+    // chunk index a workgroup stages (4 per thread, at most 512 threads)
+    {
+        const uint32_t cpr = (uint32_t)(K / 8);
+        bool found = false;
+        for (uint32_t sh = 0; sh < 24 && !found; ++sh) {
+            const uint32_t m = (uint32_t)(((1ull << sh) + cpr - 1) / cpr);
+            bool exact = true;
+            for (uint32_t c = 0; c < 4 * 512 && exact; ++c) exact = (c * m) >> sh == c / cpr;
+            if (exact) {
+                q.row_magic = m;
+                q.row_shift = sh;
+                found = true;
+            }
+        }
+        if (!found) return fail(ORBIT_EINTERNAL, "%s: no exact row division for K=%lld", who, (long long)K);
+        q.row_gap = (uint32_t)((ldx - K) * 2);
+    }
+    hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, !p->identity, info.cus, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, who);
     return ORBIT_OK;
 }

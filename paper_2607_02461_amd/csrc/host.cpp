@@ -261,34 +261,28 @@ void build_enc_table(orbit_codebook_s* c) {
     double min_gap = 2.0 * kEncRange;
     for (size_t j = 1; j < tau.size(); ++j) min_gap = std::min(min_gap, tau[j] - tau[j - 1]);
     EncTable& e = c->enc;
-    // The kernel maps u = 0 to t = center exactly (an all-zero row, for one).  The threshold at 0 is
-    // placed at that same fp32 value, and biases of threshold cells are rounded up, so an exact tie
-    // resolves to the upper code as Eq. (3)'s reading here prescribes.  w is nudged in the rare case
-    // that rounding center to fp32 would move it across a cell boundary.
-    double w = 0.9 * min_gap;
-    float center = 0.f;
-    for (int attempt = 0; attempt < 64; ++attempt, w *= 0.999) {
-        center = (float)(kEncRange / w);
-        if (std::floor((double)center) == std::floor(kEncRange / w)) break;
-    }
-    const int ncell = (int)std::ceil(2.0 * kEncRange / w) + 2;
+    // u = 0 (an all-zero row, for one) lands on t = C exactly, in the middle of cell C, where the
+    // middle threshold sits; biases of threshold cells are rounded up, so an exact tie there
+    // resolves to the upper code as Eq. (3)'s reading here prescribes.
+    const double w = 0.9 * min_gap;
+    const int C = (int)std::ceil(kEncRange / w) + 1;
+    const int ncell = 2 * C + 1;
     e.inv_w = (float)(1.0 / w);
-    e.center = center;
+    e.center = (float)C;
     e.ncell = ncell;
     e.bias.assign((size_t)ncell, 0.f);
     size_t j = 0;  // thresholds at or below the current cell start
     for (int cell = 0; cell < ncell; ++cell) {
-        const double lo = cell * w - kEncRange, hi = (cell + 1) * w - kEncRange;
+        const double lo = (cell - 0.5 - C) * w, hi = (cell + 0.5 - C) * w;
         while (j < tau.size() && tau[j] <= lo) ++j;
         const double base = (double)j;
         if (j < tau.size() && tau[j] < hi) {
-            const double T = tau[j] == 0.0 ? (double)center : (tau[j] + kEncRange) / w;
-            const double b = base + 0.5 - 0.5 * T;
+            const double b = base + 0.5 - 0.5 * (tau[j] / w);
             float bf = (float)b;
             if ((double)bf < b) bf = std::nextafter(bf, INFINITY);
             e.bias[cell] = bf;
         } else {
-            e.bias[cell] = (float)(base - 0.25 - 0.5 * cell);
+            e.bias[cell] = (float)(base - 0.5 * (cell - C));
         }
     }
 }

@@ -31,17 +31,17 @@ struct orbit_plan_s {
     uint32_t* dev_meta[orbit::kMaxDevices] = {};
 };
 
-// Encoder lookup table over the normalized coordinate u in [-kEncRange, kEncRange]: cell c covers
-// u in [c*w - kEncRange, (c+1)*w - kEncRange) with w below the smallest threshold spacing, so a cell
-// holds at most one threshold.  In cell coordinates t = (u + kEncRange) / w the code is
-// round-to-nearest-even(0.5*t + bias[cell]) with
-//     bias = base + 0.5 - 0.5*T          in a cell whose threshold sits at T (code base or base+1),
-//     bias = base - 0.25 - 0.5*c         in a cell without one (0.5*t + bias stays within 0.25 of base),
+// Encoder lookup table over the normalized coordinate u in [-kEncRange, kEncRange].  In cell
+// coordinates t = u / w + C, with w below the smallest threshold spacing and C an integer, cell c
+// covers t in [c - 0.5, c + 0.5) (the kernel rounds t to the nearest integer), so a cell holds at
+// most one threshold.  The code is round-to-nearest-even(0.5*(t - C) + bias[cell]) with
+//     bias = base + 0.5 - 0.5*tau/w      in a cell holding threshold tau (code base or base+1),
+//     bias = base - 0.5*(c - C)          in a cell without one (the value stays within 0.25 of base),
 // where base is the number of thresholds below the cell.
 constexpr double kEncRange = 1.001;  // |u| <= 1 up to rounding
 struct EncTable {
     float inv_w = 0.f;   // 1 / w
-    float center = 0.f;  // kEncRange / w
+    float center = 0.f;  // C, the cell of u = 0 (an integer)
     int32_t ncell = 0;
     std::vector<float> bias;
 };

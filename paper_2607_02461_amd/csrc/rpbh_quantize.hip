@@ -24,10 +24,11 @@
 //                v_fmac_f32_dpp computing own + sign*partner.  That leaves the upper lane of each
 //                pair holding the negated output; the sign is fixed per lane,
 //                sigma = (-1)^popcount(q), and is folded into the per-row encoder scale;
-//   encode       t = fma(z, a, c) maps the coordinate to cells of a table in LDS whose cells are
-//                narrower than the smallest gap between thresholds; with the cell's bias b,
-//                y = fma(t, 0.5, b) lies within 0.25 of the code away from the cell's threshold
-//                (if it has one) and crosses code + 0.5 exactly at it;
+//   encode       fma(z, a, C + 2^23) rounds the coordinate to its cell of a table in LDS whose cells
+//                are narrower than the smallest gap between thresholds, the index sitting in the
+//                low mantissa bits; with the cell's bias b, y = fma(z, a/2, b) lies within 0.25 of
+//                the code away from the cell's threshold (if it has one) and crosses code + 0.5
+//                exactly at it;
 //   pack         v_cvt_pk_u8_f32 rounds y to the code and inserts it as one byte of a word;
 //                a few shift-ors close the gaps, and 32 codes leave as one 4*b-byte vector store.
 // Blocks larger than 128 (h = 128 * 2^m, up to 4096): Sylvester H_h = (H_{2^m} (x) I_128)(I_{2^m} (x)
@@ -54,7 +55,6 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kEncOff = 32768;  // byte offset of the encoder table (the row buffer comes first)
 
 template <int CTRL>
 __device__ __forceinline__ float quad_perm(float v) {
@@ -132,36 +132,19 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
 }
 
-// First butterfly stage of eight bf16 pairs (y0, y1) = P[B .. B+7]: y0 + y1 and y0 - y1 as the
-// three-operand v_dot2_f32_bf16 against (1, 1) held in an SGPR, with neg_hi giving (1, -1), into
-// Z[2B .. 2B+15].  (The accumulating two-operand form the compiler picks would need its destination
-// zeroed first.)  A DOT result needs wait states before another VALU op may read it, and the
-// compiler's hazard tracking does not look inside asm, so the block ends with an s_nop covering
-// them; the outputs are early-clobber because the block writes some before it reads the rest.
-#define ORBIT_STAGE1_8(Z, P, B, ONE)                                                               \
-    asm("v_dot2_f32_bf16 %0, %16, %24, 0\n"                                                        \
-        "v_dot2_f32_bf16 %1, %16, %24, 0 neg_hi:[0,1,0]\n"                                         \
-        "v_dot2_f32_bf16 %2, %17, %24, 0\n"                                                        \
-        "v_dot2_f32_bf16 %3, %17, %24, 0 neg_hi:[0,1,0]\n"                                         \
-        "v_dot2_f32_bf16 %4, %18, %24, 0\n"                                                        \
-        "v_dot2_f32_bf16 %5, %18, %24, 0 neg_hi:[0,1,0]\n"                                         \
-        "v_dot2_f32_bf16 %6, %19, %24, 0\n"                                                        \
-        "v_dot2_f32_bf16 %7, %19, %24, 0 neg_hi:[0,1,0]\n"                                         \
-        "v_dot2_f32_bf16 %8, %20, %24, 0\n"                                                        \
-        "v_dot2_f32_bf16 %9, %20, %24, 0 neg_hi:[0,1,0]\n"                                         \
-        "v_dot2_f32_bf16 %10, %21, %24, 0\n"                                                       \
-        "v_dot2_f32_bf16 %11, %21, %24, 0 neg_hi:[0,1,0]\n"                                        \
-        "v_dot2_f32_bf16 %12, %22, %24, 0\n"                                                       \
-        "v_dot2_f32_bf16 %13, %22, %24, 0 neg_hi:[0,1,0]\n"                                        \
-        "v_dot2_f32_bf16 %14, %23, %24, 0\n"                                                       \
-        "v_dot2_f32_bf16 %15, %23, %24, 0 neg_hi:[0,1,0]\n"                                        \
-        "s_nop 4"                                                                                  \
-        : "=&v"(Z[2 * B + 0]), "=&v"(Z[2 * B + 1]), "=&v"(Z[2 * B + 2]), "=&v"(Z[2 * B + 3]),      \
-          "=&v"(Z[2 * B + 4]), "=&v"(Z[2 * B + 5]), "=&v"(Z[2 * B + 6]), "=&v"(Z[2 * B + 7]),      \
-          "=&v"(Z[2 * B + 8]), "=&v"(Z[2 * B + 9]), "=&v"(Z[2 * B + 10]), "=&v"(Z[2 * B + 11]),    \
-          "=&v"(Z[2 * B + 12]), "=&v"(Z[2 * B + 13]), "=&v"(Z[2 * B + 14]), "=&v"(Z[2 * B + 15])   \
-        : "v"(P[B + 0]), "v"(P[B + 1]), "v"(P[B + 2]), "v"(P[B + 3]), "v"(P[B + 4]),               \
-          "v"(P[B + 5]), "v"(P[B + 6]), "v"(P[B + 7]), "s"(ONE))
+// First butterfly stage from a bf16 pair (y0, y1): y0 + y1 and y0 - y1 as the three-operand
+// v_dot2_f32_bf16 against (1, 1) held in an SGPR, with neg_hi giving (1, -1).  (The accumulating
+// two-operand form the compiler picks would need its destination zeroed first.)  A DOT result
+// needs wait states before another VALU op may read it, and the compiler's hazard tracking does
+// not look inside asm, so the pair ends with an s_nop covering them.  The sum is early-clobber
+// (it is written before the pair is read again); the difference may take the pair's register.
+__device__ __forceinline__ void stage1(uint32_t P, uint32_t one_one, float& sum, float& diff) {
+    asm("v_dot2_f32_bf16 %0, %2, %3, 0\n"
+        "v_dot2_f32_bf16 %1, %2, %3, 0 neg_hi:[0,1,0]\n"
+        "s_nop 3"
+        : "=&v"(sum), "=v"(diff)
+        : "v"(P), "s"(one_one));
+}
 
 template <int BITS>
 __device__ __forceinline__ void store_packed(uint8_t* dst, const uint32_t (&w)[6]) {
@@ -285,32 +268,53 @@ struct Quantizer {
     __device__ __forceinline__ int rows_of(int g) const { return (int)min((int64_t)p.R, p.M - (int64_t)g * p.R); }
 
     // Staging: the R rows of a group sit back to back in LDS, so 16-byte chunk c of the group lands
-    // at LDS byte 16*c and takes sign-mask words 4c..4c+3 (the mask is replicated per row slot).
-    // goff[k] is the global byte offset of this lane's chunk k from the group's first row.
-    uint32_t goff[4];
+    // at byte 16*c of the row buffer, and negated at byte 16*c of its copy.  In global memory
+    // chunk c of row r lies 16*c + r*row_gap bytes past the group's first row.  With h = 128 the
+    // four offsets of a lane are loop-invariant registers (goff).  The stages across 128-blocks
+    // leave no room for them (they spilled, and each reload waited on the in-flight prefetch), so
+    // there they are recomputed per iteration; the chunk index goes through an empty asm so that
+    // the compiler cannot hoist them back out of the loop.
+    uint32_t goff[OUTER ? 1 : 4];
 
-    // The per-chunk offsets go through an empty asm so that the compiler recomputes the few
-    // address operations per iteration instead of hoisting 64-bit pointers out of the loop (which
-    // costs more registers than the loop body can spare).
+    __device__ __forceinline__ uint32_t chunk_offset(int k) const {
+        uint32_t off;
+        if constexpr (OUTER) {
+            uint32_t c = (uint32_t)(tid + k * T);
+            asm volatile("" : "+v"(c));
+            // 24-bit products (full rate): c < 2^11, row_magic < 2^20, row_gap < 2^24
+            off = c * 16u + __umul24(__umul24(c, p.row_magic) >> p.row_shift, p.row_gap);
+        } else {
+            off = goff[k];
+        }
+        // (a register of its own: built in the load's destination, which the compiler cannot
+        // prove free of the previous iteration's load, it would cost a full wait per load)
+        asm volatile("" : "+v"(off));
+        return off;
+    }
+
     __device__ __forceinline__ void load_group(int g, u32x4 (&pf)[4]) const {
         const int lim = rows_of(g) * cpr;
         const char* base = (const char*)p.X + (int64_t)g * p.R * p.ldx * 2;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            uint32_t off = goff[k];
-            asm volatile("" : "+v"(off));
+            const uint32_t off = chunk_offset(k);
             if (tid + k * T < lim) pf[k] = __builtin_nontemporal_load((const u32x4*)(base + off));
         }
     }
 
-    // applies the Rademacher sign masks of the staged positions and writes the group to LDS
+    // writes the group to LDS as it is and with every bf16 sign flipped: the gather of a position
+    // whose Rademacher sign is -1 reads the flipped copy, so the signs cost no work in the loop
     __device__ __forceinline__ void store_group(int g, const u32x4 (&pf)[4]) const {
         const int lim = rows_of(g) * cpr;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             int c = tid + k * T;
             asm volatile("" : "+v"(c));
-            if (c < lim) *(u32x4*)(smem + 16 * c) = pf[k] ^ *(const u32x4*)(p.smask + 4 * c);
+            if (c < lim) {
+                unsigned char* dst = smem + p.row_off + 16 * c;
+                *(u32x4*)dst = pf[k];
+                *(u32x4*)(dst + p.neg_off) = pf[k] ^ 0x80008000u;
+            }
         }
     }
 
@@ -339,7 +343,7 @@ struct Quantizer {
         // Block partials.  With direct loads the iteration has a single barrier, so the partials
         // alternate between two buffers: a wave writes the next group's partials only after the
         // barrier that every wave passes once it has finished reading this group's.
-        float* part = (float*)(smem + kEncOff + p.ncell * 4) + (GATHER ? 0 : (it & 1) * p.R * nb);
+        float* part = (float*)(smem + p.part_off) + (GATHER ? 0 : (it & 1) * p.R * nb);
 
         // element pairs: element 2i in the low half, 2i+1 in the high half of P[i]
         uint32_t P[16];
@@ -366,10 +370,11 @@ struct Quantizer {
 
         float z[32];
         float ss = 0.f;
-        ORBIT_STAGE1_8(z, P, 0, p.one_one);
-        ORBIT_STAGE1_8(z, P, 8, p.one_one);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) ss = dot2(P[i], P[i], ss);
+        for (int i = 0; i < 16; ++i) {
+            stage1(P[i], p.one_one, z[2 * i], z[2 * i + 1]);
+            ss = dot2(P[i], P[i], ss);
+        }
 #pragma unroll
         for (int s = 2; s < 32; s <<= 1) {
 #pragma unroll
@@ -412,7 +417,7 @@ struct Quantizer {
                 // h = 4096: the last stage pairs lanes 64 apart, in two waves.  The staging buffer
                 // is free once every wave has passed the barrier above (all gathers are done); it
                 // holds half of the lanes' values at a time.
-                float* xb = (float*)smem;
+                float* xb = (float*)(smem + p.row_off);
                 const float sgn = (tid & 64) ? -1.f : 1.f;
 #pragma unroll
                 for (int hf = 0; hf < 2; ++hf) {
@@ -457,17 +462,22 @@ struct Quantizer {
                 ((float*)p.norm)[row0 + rg] = s;
         }
 
-        // u = z / (s + eps) with z = z_unnormalised / sqrt(h); t = u / w + center is the cell
-        // coordinate and round(0.5 t + bias[cell]) the code
-        // (the floor keeps t finite, so the table index stays in range, for any eps >= 0)
-        const float a = sigma * p.enc_inv_w * __builtin_amdgcn_rcpf(fmaxf(s + p.eps, 1e-30f) * p.sqrt_h);  // 1-ulp rcp
-        const float c = p.enc_center;
-        const float* tab = (const float*)(smem + kEncOff);
+        // u = z / (s + eps) with z = z_unnormalised / sqrt(h); t = u / w + C is the cell coordinate
+        // and round(0.5 (t - C) + bias[cell]) the code.  Adding 2^23 rounds t to the cell index in
+        // the low mantissa bits, so the index costs no conversion.  The index stays inside the
+        // table: |u| <= 1 for finite rows (the floor keeps the scale finite for any eps >= 0);
+        // lanes that store nothing take a zero scale; and the 16-bit field is 0 for an infinite
+        // or NaN t (a row holding Inf or NaN: widened bf16 NaNs and the default NaN have zero low
+        // bits), whose codes are then unspecified.
+        const float a = owner ? sigma * p.enc_inv_w * __builtin_amdgcn_rcpf(fmaxf(s + p.eps, 1e-30f) * p.sqrt_h) : 0.f;  // 1-ulp rcp
+        const float ah = 0.5f * a;
+        const float cm = p.enc_center + 8388608.0f;
+        const float* tab = (const float*)smem;
         float y[32];
 #pragma unroll
         for (int r = 0; r < 32; ++r) {
-            const float t = fmaf(z[r], a, c);
-            y[r] = fmaf(t, 0.5f, tab[(uint32_t)t]);
+            const uint32_t cell = __float_as_uint(fmaf(z[r], a, cm)) & 0xFFFFu;
+            y[r] = fmaf(z[r], ah, tab[cell]);
         }
         uint32_t w[6];
         pack_codes<BITS>(y, w);
@@ -528,24 +538,27 @@ __global__ __launch_bounds__(512, 4) void rpbh_quantize_kernel(QuantParams p) {
         }
     }
     // encoder table -> LDS
-    float* tab = (float*)(smem + kEncOff);
+    float* tab = (float*)smem;
     for (int i = Q.tid; i < p.ncell; i += Q.T) tab[i] = p.enc[i];
 
     u32x4 pf[4] = {};
     if constexpr (GATHER) {
+        if constexpr (!OUTER) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int c = Q.tid + k * Q.T, r = c / Q.cpr;
-            Q.goff[k] = (uint32_t)(r * p.ldx * 2 + (c - r * Q.cpr) * 16);
+            for (int k = 0; k < 4; ++k) {
+                const int c = Q.tid + k * Q.T, r = c / Q.cpr;
+                Q.goff[k] = (uint32_t)(r * p.ldx * 2 + (c - r * Q.cpr) * 16);
+            }
         }
         const uint4* src = (const uint4*)(p.meta + Q.blk * 128 + Q.q * 32);
-        const uint32_t rowoff = (uint32_t)(Q.rg * p.K * 2);
+        const uint32_t rowoff = p.row_off + (uint32_t)(Q.rg * p.K * 2);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const uint4 v = src[i];
             const uint32_t m[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-            for (int k = 0; k < 4; ++k) Q.addr[4 * i + k] = Q.active ? rowoff + m[k] : 0u;
+            for (int k = 0; k < 4; ++k)
+                Q.addr[4 * i + k] = Q.active ? rowoff + (m[k] & 0x7FFFFFFFu) + ((m[k] >> 31) ? p.neg_off : 0u) : p.row_off;
         }
         if (blockIdx.x < p.ngroups) {
             Q.load_group(blockIdx.x, pf);
@@ -579,21 +592,28 @@ hipError_t set_smem_limit() {
 
 }  // namespace
 
-size_t quant_smem_bytes(int K, int R, int ncell) {
-    const int nb = K / 128;
-    // row buffer, encoder table, two sets of block partials (the direct-load path alternates them)
-    return (size_t)kEncOff + (size_t)ncell * 4 + (size_t)R * nb * 8 + (size_t)R * 4;
-}
-
 int quant_rows_per_group(int K) {
     const int nb = K / 128;
     return nb >= 128 ? 1 : 128 / nb;
 }
 
-hipError_t launch_rpbh_quantize(const QuantParams& p, int bits, bool norm_bf16, bool gather, int grid,
-                                hipStream_t stream) {
+hipError_t launch_rpbh_quantize(QuantParams p, int bits, bool norm_bf16, bool gather, int cus, hipStream_t stream) {
     const int threads = ((p.R * p.nb * 4 + 63) / 64) * 64;
-    const size_t smem = quant_smem_bytes(p.K, p.R, p.ncell);
+    // LDS: encoder table, two sets of block partials (the direct-load path alternates them), then
+    // the staged rows and their negated copy (the gather path), or the exchange buffer of the
+    // last h = 4096 stage (64 bytes per thread)
+    auto align16 = [](uint32_t b) { return (b + 15u) & ~15u; };
+    p.part_off = align16((uint32_t)p.ncell * 4u);
+    p.row_off = p.part_off + align16((uint32_t)(p.R * p.nb) * 8u);
+    const uint32_t rows = (uint32_t)(p.R * p.K) * 2u;
+    p.neg_off = rows;
+    const uint32_t row_bytes = gather ? 2u * rows : 0u;
+    const uint32_t xchg = p.outer > 4 ? (uint32_t)threads * 64u : 0u;
+    const size_t smem = (size_t)p.row_off + (row_bytes > xchg ? row_bytes : xchg);
+    if (smem > 160u * 1024u) return hipErrorInvalidValue;
+    // persistent: as many workgroups as fit a compute unit by LDS, at most two
+    const int per_cu = smem * 2 <= 160u * 1024u ? 2 : 1;
+    const int grid = (int)(p.ngroups < (int64_t)cus * per_cu ? p.ngroups : (int64_t)cus * per_cu);
 #define ORBIT_LAUNCH(B, NB, OU, GA)                                                                \
     do {                                                                                           \
         const hipError_t e = set_smem_limit<B, NB, OU, GA>();                                      \
