@@ -465,19 +465,20 @@ struct Quantizer {
         // u = z / (s + eps) with z = z_unnormalised / sqrt(h); t = u / w + C is the cell coordinate
         // and round(0.5 (t - C) + bias[cell]) the code.  Adding 2^23 rounds t to the cell index in
         // the low mantissa bits, so the index costs no conversion.  The index stays inside the
-        // table: |u| <= 1 for finite rows (the floor keeps the scale finite for any eps >= 0);
-        // lanes that store nothing take a zero scale; and the 16-bit field is 0 for an infinite
-        // or NaN t (a row holding Inf or NaN: widened bf16 NaNs and the default NaN have zero low
-        // bits), whose codes are then unspecified.
+        // table for every finite row (|u| <= 1; the floor keeps the scale finite for any eps >= 0),
+        // and lanes that store nothing take a zero scale.  A row holding Inf or NaN has
+        // unspecified codes (its lookups may read outside the table, which returns zero).
         const float a = owner ? sigma * p.enc_inv_w * __builtin_amdgcn_rcpf(fmaxf(s + p.eps, 1e-30f) * p.sqrt_h) : 0.f;  // 1-ulp rcp
         const float ah = 0.5f * a;
         const float cm = p.enc_center + 8388608.0f;
-        const float* tab = (const float*)smem;
+        // f = C + 2^23 + round(t - C) has the bit pattern 0x4B000000 + cell, so the cell's LDS byte
+        // address is 4 * bits(f) + (table - 4 * 0x4B000000) (mod 2^32): one shift-add
+        const uint32_t tab = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem - 0x2C000000u;
         float y[32];
 #pragma unroll
         for (int r = 0; r < 32; ++r) {
-            const uint32_t cell = __float_as_uint(fmaf(z[r], a, cm)) & 0xFFFFu;
-            y[r] = fmaf(z[r], ah, tab[cell]);
+            const uint32_t addr = __float_as_uint(fmaf(z[r], a, cm)) * 4u + tab;
+            y[r] = fmaf(z[r], ah, *(const __attribute__((address_space(3))) float*)(uintptr_t)addr);
         }
         uint32_t w[6];
         pack_codes<BITS>(y, w);
