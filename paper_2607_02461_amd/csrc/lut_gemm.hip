@@ -476,6 +476,22 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
             }
         }
     const bool plain = !p.bias && !p.gelu && !p.out_bf16;
+    // bf16 bias of the lane's columns, loaded once for its four rows (zero without a bias)
+    uint2 bv[2][4];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t c = col0 + j * 32 + 8 * q;
+            if (p.bias && c + 3 < p.N && p.vec4) {
+                bv[j][q] = *(const uint2*)(p.bias + c);
+            } else {
+                uint16_t v[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = p.bias && c + r < p.N ? p.bias[c + r] : (uint16_t)0;
+                bv[j][q] = make_uint2(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16));
+            }
+        }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int64_t row = m0 + wm * 128 + i * 32 + (lane & 31);
@@ -497,9 +513,11 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
                     continue;
                 }
                 if (!plain) {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        v[r] = epilogue_value(p, v[r], p.bias && c + r < p.N ? bf16_to_f32(p.bias[c + r]) : 0.f);
+                    const uint2 b = bv[j][q];
+                    v[0] = epilogue_value(p, v[0], __uint_as_float(b.x << 16));
+                    v[1] = epilogue_value(p, v[1], __uint_as_float(b.x & 0xFFFF0000u));
+                    v[2] = epilogue_value(p, v[2], __uint_as_float(b.y << 16));
+                    v[3] = epilogue_value(p, v[3], __uint_as_float(b.y & 0xFFFF0000u));
                 }
                 if (full && p.out_bf16) {
                     *(uint2*)((uint16_t*)p.Y + row * p.ldy + c) =
