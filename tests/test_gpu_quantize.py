@@ -283,3 +283,25 @@ def test_zero_row_gives_zero_output_row():
     Y = oq.orbit_qlinear(cb, xc, xn, cb, wc, wn)
     torch.cuda.synchronize()
     assert torch.all(Y[3] == 0) and torch.all(Y[[0, 1, 2, 4]].abs().sum(dim=1) > 0)
+
+
+@pytest.mark.parametrize("h", [128, 1024])
+@pytest.mark.parametrize("weights", [False, True])
+def test_extreme_coordinates(h, weights):
+    # Rows whose rotated image is (up to bf16 rounding of the input) a single coordinate of
+    # magnitude ||x||: the normalized coordinate reaches +-1 and the encoder looks up the last
+    # cells at both ends of its table, while every other coordinate sits at the middle
+    # threshold's cell.  Built with the oracle's inverse RPBH, at magnitudes from 2^-60 to 2^60,
+    # plus the same rows with small noise added.
+    K, seed = 3072, 5
+    op = oracle.rpbh_plan(K, h, seed)
+    idx = [0, 1, 127, 128, 1023, 1024, 2047, 3071]
+    E = np.zeros((2 * len(idx), K))
+    for r, i in enumerate(idx):
+        E[2 * r, i], E[2 * r + 1, i] = 1.0, -1.0
+    base = oracle.rpbh_inverse(E, op)
+    rows = [base * 2.0 ** s for s in (-60, -10, 0, 10, 60)]
+    noisy = base + 1e-3 * np.random.default_rng(3).standard_normal(base.shape)
+    X = torch.from_numpy(np.concatenate(rows + [noisy]).astype(np.float32)).to(torch.bfloat16).to(DEV)
+    for bits in (4,) if weights else (2, 3, 4, 6):
+        compare_quantizer(f"extreme coordinates h={h}", X, bits, seed=seed, weights=weights, h=h, oplan=op)
