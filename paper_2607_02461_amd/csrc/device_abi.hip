@@ -147,22 +147,17 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     q.outer = 0;
     while ((kQuantH << q.outer) < p->h) ++q.outer;
     q.sqrt_h = (float)std::sqrt((double)p->h);
-    // row of a staged chunk: an exact multiply-shift division by the chunks per row for every
-    // chunk index a workgroup stages (4 per thread, at most 512 threads)
+    // row of a staged chunk: an exact multiply-shift division by the chunks per row d for every
+    // chunk index a workgroup stages (4 per thread, at most 512 threads: below 2^11).  With
+    // s = 11 + ceil(log2 d) and m = ceil(2^s / d), m d - 2^s < d <= 2^(s - 11), so
+    // floor(c m / 2^s) = floor(c / d) for c < 2^11 (Granlund and Montgomery, PLDI 1994); c m stays
+    // below 2^24 for the kernel's 24-bit multiply.
     {
         const uint32_t cpr = (uint32_t)(K / 8);
-        bool found = false;
-        for (uint32_t sh = 0; sh < 24 && !found; ++sh) {
-            const uint32_t m = (uint32_t)(((1ull << sh) + cpr - 1) / cpr);
-            bool exact = true;
-            for (uint32_t c = 0; c < 4 * 512 && exact; ++c) exact = (c * m) >> sh == c / cpr;
-            if (exact) {
-                q.row_magic = m;
-                q.row_shift = sh;
-                found = true;
-            }
-        }
-        if (!found) return fail(ORBIT_EINTERNAL, "%s: no exact row division for K=%lld", who, (long long)K);
+        uint32_t lg = 0;
+        while ((1u << lg) < cpr) ++lg;
+        q.row_shift = 11 + lg;
+        q.row_magic = (uint32_t)(((1ull << q.row_shift) + cpr - 1) / cpr);
         q.row_gap = (uint32_t)((ldx - K) * 2);
     }
     hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, !p->identity, info.cus, (hipStream_t)stream);
