@@ -145,7 +145,8 @@ void lloydmax_codebook_destroy(orbit_codebook c);
  *
  * Pointers: W and w_codes 16-byte aligned, w_norm 2-byte aligned.
  * Errors: ORBIT_EINVAL (null pointer, K mismatch, ldw, alignment); ORBIT_EUNSUPPORTED
- * (h outside 128..4096, K > 16384, bits not in {2, 3, 4, 6}, more than 2^31 - 1 rows);
+ * (h outside 128..4096, K > 16384, bits not in {2, 3, 4, 6}, more than 2^31 - 1 rows, a row
+ * stride ldw - K of 2^23 elements or more);
  * ORBIT_EHIP.  N = 0 returns at once.  Packing as above: at b = 6 every 4 codes fill 3 bytes.
  */
 orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const uint16_t* W, int64_t N,
@@ -165,9 +166,9 @@ orbit_status quantize_weights_offline(orbit_plan p, orbit_codebook cb_w, const u
  *   x_norm  device, fp32 [M]: s_n (the dequantized row is s_n * L_a[code_n])
  *
  * Pointers: X and x_codes 16-byte aligned, x_norm 4-byte aligned.
- * Errors and limits as for quantize_weights_offline; also ORBIT_EUNSUPPORTED for ldx - K of
- * 2^23 elements or more.  M = 0 returns at once.  A row holding Inf or NaN gets a non-finite
- * norm and unspecified codes (both entry points); other rows are unaffected.
+ * Errors and limits as for quantize_weights_offline.  M = 0 returns at once.  A row holding Inf
+ * or NaN gets a non-finite norm and unspecified codes (both entry points); other rows are
+ * unaffected.
  */
 orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t* X, int64_t M, int64_t K,
                                int64_t ldx, float eps, uint8_t* x_codes, float* x_norm, void* stream);

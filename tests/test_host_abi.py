@@ -238,3 +238,18 @@ def test_adaln_calls_validate_before_launch():
     # empty calls succeed without touching the device
     assert _status(lib.adaln_int4_linear, null, 0, 128, null, null, 16, 128, null, null, 16, null)[0] == oq.ORBIT_OK
     assert _status(lib.adaln_int4_quantize_weights, null, 0, 128, 128, null, null, null)[0] == oq.ORBIT_OK
+
+
+def test_quantizer_rejects_row_gaps_of_2_23_elements():
+    # the staging offsets use 24-bit products of the byte gap between rows: ld - K must stay
+    # below 2^23 elements, for activations and weights alike (checked before any device work)
+    lib = oq.lib()
+    p = oq.rpbh_plan(256, 128, 0)
+    cb = oq.lloydmax_codebook(4, 256)
+    null, fake = ctypes.c_void_p(0), ctypes.c_void_p(1 << 20)
+    st, msg = _status(lib.rpbh_quantize_act, p.handle, cb.handle, fake, 4, 256, 256 + (1 << 23), 1e-10, fake, fake,
+                      null)
+    assert st == oq.ORBIT_EUNSUPPORTED and "stride" in msg
+    st, msg = _status(lib.quantize_weights_offline, p.handle, cb.handle, fake, 4, 256, 256 + (1 << 23), 1e-10, fake,
+                      fake, null)
+    assert st == oq.ORBIT_EUNSUPPORTED and "stride" in msg
