@@ -37,7 +37,7 @@ struct QuantParams {
     const float* enc;      // encoder table: per-cell bias (see the codebook's encoder table)
     int ncell;
     float enc_inv_w;       // cells per unit of the normalized coordinate
-    float enc_center;      // cell coordinate of u = 0
+    float enc_center;      // C: the (integer) cell of u = 0
     uint32_t one_one;      // bf16 pair (1.0, 1.0), 0x3F803F80
     int outer;             // log2(h / 128): Hadamard stages across 128-blocks (0 for h = 128)
     float sqrt_h;          // sqrt(h), the FWHT's normalization

@@ -4,18 +4,18 @@
 // weight pass (Sec. 4.2, Eqs. (4)-(6)); they differ only in the type of the stored norm.
 //
 // Work mapping (h = 128).  A persistent workgroup owns R rows per iteration and loops over row
-// groups.  Rows are staged in LDS as raw bf16 with 16-byte coalesced loads.  The next group is
-// loaded into registers right after the current group's gathers and written over the staging
-// buffer at the end of the iteration, so the HBM reads overlap the butterflies, the norm
-// reduction and the encoder, and the gather offsets stay loop-invariant registers.  Every
-// 128-block of a row belongs to one quad of lanes; lane q of the quad holds the 32 consecutive
-// post-permutation positions q*32 .. q*32+31.
+// groups.  Rows are staged in LDS with 16-byte coalesced loads, twice: as loaded and with every
+// bf16 sign bit flipped.  The next group is loaded into registers right after the current
+// group's gathers and written over the staging buffers at the end of the iteration, so the HBM
+// reads overlap the butterflies, the norm reduction and the encoder, and the gather offsets stay
+// loop-invariant registers.  Every 128-block of a row belongs to one quad of lanes; lane q of the
+// quad holds the 32 consecutive post-permutation positions q*32 .. q*32+31.  (With an identity
+// permutation there is no staging: each lane loads its 64 contiguous bytes straight from HBM.)
 //
 // Per element the hot loop costs:
-//   gather       one LDS u16 read through a per-lane table of byte offsets (the permutation);
-//   sign         the Rademacher signs are XORed into the bf16 sign bits of the staged words (the
-//                plan carries a per-source-position mask, sign of the position the element moves
-//                to), half an op per element;
+//   gather       one LDS u16 read through a per-lane table of byte offsets (the permutation),
+//                each pointing into the copy the position's Rademacher sign selects;
+//   sign         the flipped copy: half an XOR per element while staging;
 //   widening and the first butterfly stage together: one v_dot2_f32_bf16 of a gathered bf16
 //                pair (y0, y1) with (1, 1) or (1, -1) gives y0 + y1 or y0 - y1 exactly in fp32;
 //   row norm     half a v_dot2 (the pair against itself; the rotation is orthogonal, so the sum of
