@@ -236,13 +236,15 @@ def main():
     L0 = layers[0]
     K0 = L0["lin"].K
 
-    def time_quant(plan_v, reps=10):
+    def time_quant(plan_v, reps=10, X=None, cb=None, xc=None, xn=None):
+        X = L0["X"] if X is None else X
+        cb, xc, xn = (L0["cba"], L0["xc"], L0["xn"]) if cb is None else (cb, xc, xn)
         for _ in range(2):
-            oq.rpbh_quantize_act(plan_v, L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
+            oq.rpbh_quantize_act(plan_v, cb, X, 1e-10, xc, xn)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(reps):
-            oq.rpbh_quantize_act(plan_v, L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
+            oq.rpbh_quantize_act(plan_v, cb, X, 1e-10, xc, xn)
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps
@@ -272,6 +274,22 @@ def main():
     rot["dense_haar_rotation_gemm_ms"] = e0.elapsed_time(e1) / 5
     rot["shape"] = f"{L0['lin'].M} x {K0}"
     del Qt, Xr
+    # Full RHT (one Hadamard block over the whole row, no permutation) needs a power-of-two d: the
+    # first 4096 channels of the same input (a strided view), against RPBH and Block-RHT there
+    K1 = 4096
+    X1 = L0["X"][:, :K1]
+    cb1 = oq.lloydmax_codebook(L0["lin"].ba, K1)
+    xc1 = torch.empty((L0["lin"].M, K1 * L0["lin"].ba // 8), dtype=torch.uint8, device=dev)
+    xn1 = torch.empty((L0["lin"].M,), dtype=torch.float32, device=dev)
+    d4 = {"shape": f"{L0['lin'].M} x {K1}"}
+    for hh in (128, K1):
+        pr = oq.rpbh_plan(K1, hh, wl.plan_seed)
+        _, signs = pr.arrays()
+        pb = oq.rpbh_plan_from_arrays(K1, hh, np.arange(K1), signs)
+        d4[f"rpbh_h{hh}_ms"] = time_quant(pr, X=X1, cb=cb1, xc=xc1, xn=xn1)
+        d4[f"{'full_rht' if hh == K1 else 'block_rht'}_h{hh}_ms"] = time_quant(pb, X=X1, cb=cb1, xc=xc1, xn=xn1)
+    rot["d4096"] = d4
+    del xc1, xn1
 
     # NEXT row: the up-projection with the MLP's GELU and a bf16 output fused into the epilogue
     # (the form that feeds the next quantizer), against the plain fp32 GEMM on the same codes
