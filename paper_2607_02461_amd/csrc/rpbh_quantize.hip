@@ -409,7 +409,14 @@ struct Quantizer {
         }
         ss += quad_perm<kQuadXor1>(ss);
         ss += quad_perm<kQuadXor2>(ss);
-        if (owner && q == 0) part[rg * nb + blk] = ss;
+        if (owner && q == 0) {
+            // rg * nb + blk is the lane's task, tid / 4: recomputed here (the empty asm keeps it
+            // from being hoisted), since a register held across the loop spilled with h > 128 and
+            // its reload waited for the in-flight prefetch
+            int task = tid >> 2;
+            asm volatile("" : "+v"(task));
+            part[task] = ss;
+        }
         __syncthreads();
 
         if constexpr (OUTER) {
