@@ -208,7 +208,8 @@ orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const fl
  *     Y[n][i] = act(x_norm[n] * w_norm[i] * sum_k L_a[...] * L_w[...] + bias[i])
  *
  *   bias       device, bf16 [N], or NULL for none (Eq. (1) itself has no bias)
- *   act        ORBIT_ACT_NONE, or ORBIT_ACT_GELU: x * Phi(x) with the exact error function
+ *   act        ORBIT_ACT_NONE, or ORBIT_ACT_GELU: x * Phi(x), Phi the standard normal CDF from
+ *              erfc to a fractional error below 1.2e-7 (Numerical Recipes' Chebyshev-fitted form)
  *   out_dtype  ORBIT_OUT_F32, or ORBIT_OUT_BF16 (round to nearest even), the input type of
  *              rpbh_quantize_act
  *   Y          device, [M][ldy] elements of out_dtype

@@ -66,7 +66,7 @@ struct GemmParams {
     int K;
     int vec4;              // Y, ldy, wn and bias allow 4-wide row stores and loads
     const uint16_t* bias;  // bf16 [N] or null, added after the rescaling
-    int gelu;              // apply x * Phi(x) (exact erf) after the bias
+    int gelu;              // apply x * Phi(x) (erfc to 1.2e-7 fractional error) after the bias
     int out_bf16;          // store Y as bf16 (round to nearest even) instead of fp32
     uint16_t lut_a[64];    // fp16 levels (2^ba used)
     uint16_t lut_w[16];    // fp16 levels (2^bw used)

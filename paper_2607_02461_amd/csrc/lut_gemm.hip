@@ -172,10 +172,39 @@ __device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
     return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-// The rest of the layer after the rescaled contraction: bias, then GELU (x * Phi(x), exact erf).
+// GELU(v) = v * Phi(v), Phi the standard normal CDF, with Phi from the complementary error
+// function: Phi(v) = 1 - q for v >= 0 and q for v < 0, q = erfc(|v|/sqrt(2)) / 2.  erfc is the
+// Chebyshev-fitted form of Numerical Recipes in C (2nd ed., Sec. 6.2, erfcc): for x >= 0,
+//     erfc(x) = t exp(-x^2 + P(t)),  t = 1 / (1 + x/2),  P a degree-9 polynomial,
+// with fractional error below 1.2e-7 everywhere, so GELU keeps its relative accuracy in the
+// negative tail too.  log2(e) is folded into the coefficients (the hardware exponential is base
+// 2) and the factor 1/2 of q into the constant term.  One reciprocal, one exp2 and nine fused
+// multiply-adds without branches: on a layer's outputs (|Y| up to a few units) the library erff
+// takes several ranges whose branches diverge across a wave.
+__device__ __forceinline__ float gelu_erfc(float v) {
+    constexpr float L2E = 1.4426950408889634f;
+    constexpr float c0 = -1.26551223f * L2E - 1.f, c1 = 1.00002368f * L2E, c2 = 0.37409196f * L2E,
+                    c3 = 0.09678418f * L2E, c4 = -0.18628806f * L2E, c5 = 0.27886807f * L2E,
+                    c6 = -1.13520398f * L2E, c7 = 1.48851587f * L2E, c8 = -0.82215223f * L2E,
+                    c9 = 0.17087277f * L2E;
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.35355339059327373f, fabsf(v), 1.f));  // x = |v|/sqrt(2)
+    float P = fmaf(t, c9, c8);
+    P = fmaf(t, P, c7);
+    P = fmaf(t, P, c6);
+    P = fmaf(t, P, c5);
+    P = fmaf(t, P, c4);
+    P = fmaf(t, P, c3);
+    P = fmaf(t, P, c2);
+    P = fmaf(t, P, c1);
+    P = fmaf(t, P, c0);
+    const float q = t * __builtin_amdgcn_exp2f(fmaf(v * v, -0.5f * L2E, P));
+    return v * (v >= 0.f ? 1.f - q : q);
+}
+
+// The rest of the layer after the rescaled contraction: bias, then GELU (x * Phi(x)).
 __device__ __forceinline__ float epilogue_value(const GemmParams& p, float v, float bias) {
     v += bias;
-    if (p.gelu) v = 0.5f * v * (1.f + erff(v * 0.7071067811865476f));
+    if (p.gelu) v = gelu_erfc(v);
     return v;
 }
 
