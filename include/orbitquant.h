@@ -26,7 +26,8 @@
  *     at once.  The first device call that uses a plan on a device uploads the plan's
  *     permutation/sign table to that device (d*4 bytes, hipMalloc + synchronous copy) and
  *     keeps it until the handle is destroyed.  Destroy a handle only after the work that
- *     uses it has finished.
+ *     uses it has finished.  Make that first call outside stream capture; later calls record
+ *     only kernel launches and can be captured in a HIP graph and replayed.
  */
 #ifndef ORBITQUANT_H
 #define ORBITQUANT_H

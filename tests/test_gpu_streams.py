@@ -1,0 +1,91 @@
+"""Streams and graph capture through the C ABI: device calls only enqueue on the caller's stream,
+handles may be shared by calls on several streams at once, and once a plan and codebook have been
+used on the device (their tables uploaded), the quantizer and the layer can be captured in a HIP
+graph and replayed.  Every kernel is deterministic, so each result is compared bit for bit with the
+same call made eagerly on the default stream."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2607_02461_amd as oq
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _bf16(M, K, seed, scale=1.0):
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    return (torch.randn((M, K), generator=g, device=DEV) * scale).to(torch.bfloat16)
+
+
+def _layer(X, W, plan, cb, bias=None, gelu=False, out_dtype=torch.float32):
+    xc, xn = oq.rpbh_quantize_act(plan, cb, X)
+    wc, wn = oq.quantize_weights_offline(plan, cb, W)
+    Y = oq.orbit_qlinear_ex(cb, xc, xn, cb, wc, wn, bias=bias, gelu=gelu, out_dtype=out_dtype)
+    return xc, xn, wc, wn, Y
+
+
+def test_two_streams_share_handles():
+    # two layers on two non-default streams at once, the same plan and codebook handles, against
+    # the same calls made one after the other on the default stream
+    K = 3072
+    plan, cb = oq.rpbh_plan(K, 128, 0), oq.lloydmax_codebook(4, K)
+    Xs = [_bf16(4099, K, 1), _bf16(2311, K, 2, scale=3.0)]
+    Ws = [_bf16(3072, K, 3, scale=0.02), _bf16(5000, K, 4, scale=0.02)]
+    ref = [_layer(X, W, plan, cb) for X, W in zip(Xs, Ws)]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    out = [None, None]
+    for i in range(2):
+        streams[i].wait_stream(torch.cuda.current_stream())
+    for _ in range(3):   # several rounds, so the two streams' kernels overlap
+        for i in range(2):
+            with torch.cuda.stream(streams[i]):
+                out[i] = _layer(Xs[i], Ws[i], plan, cb)
+    torch.cuda.synchronize()
+    for i in range(2):
+        for a, b in zip(out[i], ref[i]):
+            assert torch.equal(a, b), f"stream {i}: results differ from the default-stream call"
+
+
+def test_graph_capture_and_replay():
+    # quantize + fused layer (bias, GELU, bf16 output) captured once, replayed on new input
+    # contents with eager work between replays; every replay equals the eager result
+    K, M, N = 5120, 3000, 4096
+    plan, cb = oq.rpbh_plan(K, 128, 0), oq.lloydmax_codebook(4, K)
+    W = _bf16(N, K, 9, scale=0.015)
+    wc, wn = oq.quantize_weights_offline(plan, cb, W)
+    bias = (torch.randn(N, device=DEV) * 0.1).to(torch.bfloat16)
+    X = _bf16(M, K, 10)
+    xc = torch.empty((M, K // 2), dtype=torch.uint8, device=DEV)
+    xn = torch.empty((M,), dtype=torch.float32, device=DEV)
+    Y = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+
+    def step():
+        oq.rpbh_quantize_act(plan, cb, X, 1e-10, xc, xn)
+        oq.orbit_qlinear_ex(cb, xc, xn, cb, wc, wn, bias=bias, gelu=True, out_dtype=torch.bfloat16, out=Y)
+
+    step()                       # eager first call: uploads the plan and codebook tables
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):   # warm-up on the capture stream, as torch recommends
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    for r in range(4):
+        X.copy_(_bf16(M, K, 100 + r, scale=1.0 + r))
+        g.replay()
+        torch.cuda.synchronize()
+        got = (xc.clone(), xn.clone(), Y.clone())
+        _ = _bf16(1024, 1024, 7).float().sum()       # unrelated eager work between replays
+        step()                                        # the same step, eagerly
+        torch.cuda.synchronize()
+        for a, b, name in zip(got, (xc, xn, Y), ("codes", "norms", "Y")):
+            assert torch.equal(a, b), f"replay {r}: {name} differ from the eager step"
