@@ -24,7 +24,7 @@
  *     and happen before any launch; a launch failure returns ORBIT_EHIP with HIP's message.
  *   - Handles are immutable after creation and may be used from several threads and streams
  *     at once.  The first device call that uses a plan on a device uploads the plan's
- *     permutation/sign table to that device (d*4 bytes, hipMalloc + synchronous copy) and
+ *     permutation/sign tables to that device (6 bytes per input, hipMalloc + synchronous copy) and
  *     keeps it until the handle is destroyed.  Destroy a handle only after the work that
  *     uses it has finished.  Make that first call outside stream capture; later calls record
  *     only kernel launches and can be captured in a HIP graph and replayed.
