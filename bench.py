@@ -307,7 +307,40 @@ def main():
     fused_ms = e0.elapsed_time(e1) / 5
     fused = {"linear": L0["lin"].name, "epilogue": "GELU(erf) + bf16 output", "ms": fused_ms,
              "tflops": float(flops[0]) / (fused_ms * 1e-3) / 1e12, "plain_fp32_ms": float(gemm_ms[0])}
-    del Yb
+
+    # NEXT row: the MLP as a model runs it, the fused up-projection's bf16 output feeding the
+    # down-projection's quantizer directly, against the same chain with an fp32 up output, GELU
+    # and the bf16 cast as separate torch ops
+    L1 = layers[1]
+    H = Yb
+
+    def chain_fused():
+        oq.rpbh_quantize_act(L0["plan"], L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
+        oq.orbit_qlinear_ex(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], gelu=True,
+                            out_dtype=torch.bfloat16, out=H)
+        oq.rpbh_quantize_act(L1["plan"], L1["cba"], H, 1e-10, L1["xc"], L1["xn"])
+        oq.orbit_qlinear(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["Y"])
+
+    def chain_unfused():
+        oq.rpbh_quantize_act(L0["plan"], L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
+        oq.orbit_qlinear(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"])
+        H.copy_(torch.nn.functional.gelu(L0["Y"]))
+        oq.rpbh_quantize_act(L1["plan"], L1["cba"], H, 1e-10, L1["xc"], L1["xn"])
+        oq.orbit_qlinear(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["Y"])
+
+    chain = {"layers": f"{L0['lin'].name} -> GELU -> {L1['lin'].name}"}
+    for name, fn in (("fused_ms", chain_fused), ("unfused_ms", chain_unfused)):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        chain[name] = e0.elapsed_time(e1) / 3
+    chain["fused_tflops"] = float(flops[0] + flops[1]) / (chain["fused_ms"] * 1e-3) / 1e12
+    del Yb, H
 
     # NEXT row: the video recipe's 6-bit activations (W4A6, the paper's Wan setting) on the
     # up-projection: the quantizer writing 6-bit codes and the GEMM decoding them
@@ -392,6 +425,7 @@ def main():
         "quantizer_paper_block_rule": paper_h,
         "rotation_classes": rot,
         "fused_epilogue": fused,
+        "mlp_chain": chain,
         "w4a6": a6,
         "trunk_c5": trunk,
         "adaln_int4": adaln,
