@@ -107,7 +107,10 @@ def main():
         xc = torch.empty((lin.M, lin.K * lin.ba // 8), dtype=torch.uint8, device=dev)
         xn = torch.empty((lin.M,), dtype=torch.float32, device=dev)
         Y = torch.empty((lin.M, lin.N), dtype=torch.float32, device=dev)
-        layers.append(dict(lin=lin, X=X, W=W, wc=wc, wn=wn, xc=xc, xn=xn, Y=Y,
+        # the K-split workspace of a layer too small to fill the GPU (none for c4's projections)
+        wsp = torch.empty(max(16, oq.orbit_qlinear_workspace_size(lin.M, lin.N, lin.K)), dtype=torch.uint8,
+                          device=dev)
+        layers.append(dict(lin=lin, X=X, W=W, wc=wc, wn=wn, xc=xc, xn=xn, Y=Y, ws=wsp,
                            plan=plans[lin.K], cba=cbs[(lin.ba, lin.K)], cbw=cbs[(lin.bw, lin.K)]))
 
     def weight_pass():
@@ -145,7 +148,7 @@ def main():
             if ev is not None:
                 ev[4 * i + 1].record()
                 ev[4 * i + 2].record()
-            oq.orbit_qlinear(L["cba"], L["xc"], L["xn"], L["cbw"], L["wc"], L["wn"], L["Y"])
+            oq.orbit_qlinear_ws(L["cba"], L["xc"], L["xn"], L["cbw"], L["wc"], L["wn"], L["ws"], out=L["Y"])
             if ev is not None:
                 ev[4 * i + 3].record()
 
@@ -188,7 +191,9 @@ def main():
     gemm_launch_flops = float(flops.mean())
     gemm_avg_ms = float(gemm_ms.mean())
     roofline = {
-        "kernel": "lut_gemm_big" if wl is workloads.C4 else "lut_gemm_kernel",
+        "kernel": "lut_gemm_big" if wl is workloads.C4 else (
+            "lut_gemm_kernel+lut_gemm_reduce" if layers[0]["ws"].numel() > 16 else "lut_gemm_kernel"),
+        "k_splits": [L["ws"].numel() // (4 * L["lin"].M * L["lin"].N) or 1 for L in layers],
         "bound": "mfma",
         "achieved": gemm_launch_flops / (gemm_avg_ms * 1e-3) / 1e12,
         "peak": FP16_MFMA_PEAK_TFLOPS,
@@ -275,8 +280,9 @@ def main():
     rot["shape"] = f"{L0['lin'].M} x {K0}"
     del Qt, Xr
     # Full RHT (one Hadamard block over the whole row, no permutation) needs a power-of-two d: the
-    # first 4096 channels of the same input (a strided view), against RPBH and Block-RHT there
-    K1 = 4096
+    # first 4096 channels of the same input (a strided view; 2048 of c1's 3072), against RPBH and
+    # Block-RHT there
+    K1 = 4096 if K0 >= 4096 else 2048
     X1 = L0["X"][:, :K1]
     cb1 = oq.lloydmax_codebook(L0["lin"].ba, K1)
     xc1 = torch.empty((L0["lin"].M, K1 * L0["lin"].ba // 8), dtype=torch.uint8, device=dev)
@@ -288,19 +294,19 @@ def main():
         pb = oq.rpbh_plan_from_arrays(K1, hh, np.arange(K1), signs)
         d4[f"rpbh_h{hh}_ms"] = time_quant(pr, X=X1, cb=cb1, xc=xc1, xn=xn1)
         d4[f"{'full_rht' if hh == K1 else 'block_rht'}_h{hh}_ms"] = time_quant(pb, X=X1, cb=cb1, xc=xc1, xn=xn1)
-    rot["d4096"] = d4
+    rot[f"d{K1}"] = d4
     del xc1, xn1
 
     # NEXT row: the up-projection with the MLP's GELU and a bf16 output fused into the epilogue
     # (the form that feeds the next quantizer), against the plain fp32 GEMM on the same codes
     Yb = torch.empty((L0["lin"].M, L0["lin"].N), dtype=torch.bfloat16, device=dev)
     for _ in range(2):
-        oq.orbit_qlinear_ex(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], gelu=True,
+        oq.orbit_qlinear_ws(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["ws"], gelu=True,
                             out_dtype=torch.bfloat16, out=Yb)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(5):
-        oq.orbit_qlinear_ex(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], gelu=True,
+        oq.orbit_qlinear_ws(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["ws"], gelu=True,
                             out_dtype=torch.bfloat16, out=Yb)
     e1.record()
     torch.cuda.synchronize()
@@ -311,36 +317,38 @@ def main():
     # NEXT row: the MLP as a model runs it, the fused up-projection's bf16 output feeding the
     # down-projection's quantizer directly, against the same chain with an fp32 up output, GELU
     # and the bf16 cast as separate torch ops
-    L1 = layers[1]
-    H = Yb
+    chain = None
+    if len(layers) > 1:   # c4's two projections (c1 is a single linear)
+        L1 = layers[1]
+        H = Yb
 
-    def chain_fused():
-        oq.rpbh_quantize_act(L0["plan"], L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
-        oq.orbit_qlinear_ex(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], gelu=True,
-                            out_dtype=torch.bfloat16, out=H)
-        oq.rpbh_quantize_act(L1["plan"], L1["cba"], H, 1e-10, L1["xc"], L1["xn"])
-        oq.orbit_qlinear(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["Y"])
+        def chain_fused():
+            oq.rpbh_quantize_act(L0["plan"], L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
+            oq.orbit_qlinear_ex(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], gelu=True,
+                                out_dtype=torch.bfloat16, out=H)
+            oq.rpbh_quantize_act(L1["plan"], L1["cba"], H, 1e-10, L1["xc"], L1["xn"])
+            oq.orbit_qlinear(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["Y"])
 
-    def chain_unfused():
-        oq.rpbh_quantize_act(L0["plan"], L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
-        oq.orbit_qlinear(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"])
-        H.copy_(torch.nn.functional.gelu(L0["Y"]))
-        oq.rpbh_quantize_act(L1["plan"], L1["cba"], H, 1e-10, L1["xc"], L1["xn"])
-        oq.orbit_qlinear(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["Y"])
+        def chain_unfused():
+            oq.rpbh_quantize_act(L0["plan"], L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
+            oq.orbit_qlinear(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"])
+            H.copy_(torch.nn.functional.gelu(L0["Y"]))
+            oq.rpbh_quantize_act(L1["plan"], L1["cba"], H, 1e-10, L1["xc"], L1["xn"])
+            oq.orbit_qlinear(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["Y"])
 
-    chain = {"layers": f"{L0['lin'].name} -> GELU -> {L1['lin'].name}"}
-    for name, fn in (("fused_ms", chain_fused), ("unfused_ms", chain_unfused)):
-        for _ in range(2):
-            fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(3):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        chain[name] = e0.elapsed_time(e1) / 3
-    chain["fused_tflops"] = float(flops[0] + flops[1]) / (chain["fused_ms"] * 1e-3) / 1e12
-    del Yb, H
+        chain = {"layers": f"{L0['lin'].name} -> GELU -> {L1['lin'].name}"}
+        for name, fn in (("fused_ms", chain_fused), ("unfused_ms", chain_unfused)):
+            for _ in range(2):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(3):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            chain[name] = e0.elapsed_time(e1) / 3
+        chain["fused_tflops"] = float(flops[0] + flops[1]) / (chain["fused_ms"] * 1e-3) / 1e12
+    del Yb
 
     # NEXT row: the video recipe's 6-bit activations (W4A6, the paper's Wan setting) on the
     # up-projection: the quantizer writing 6-bit codes and the GEMM decoding them

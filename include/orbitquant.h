@@ -226,6 +226,36 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
                               int64_t ldy, void* stream);
 
 /*
+ * orbit_qlinear_workspace_size -- bytes of device workspace with which orbit_qlinear_ws splits
+ * the contraction over K for a layer of M x N outputs and K inputs on the current device; 0 when
+ * it would not split (a layer that already fills the device's compute units, or too short a K).
+ * A split is worth it where the grid of output tiles is small (few tokens, Sec. 5's low-batch
+ * serving): each split contracts a contiguous range of K, so one layer keeps every compute unit busy.
+ *
+ *   bytes  host, out: splits * M * N * 4 (fp32 partial sums), or 0
+ *
+ * Errors: ORBIT_EINVAL (null bytes, negative M or N, K not a positive multiple of 64 up to
+ * 2^30); ORBIT_EHIP (no device).  M = 0 or N = 0 gives 0.
+ */
+orbit_status orbit_qlinear_workspace_size(int64_t M, int64_t N, int64_t K, size_t* bytes);
+
+/*
+ * orbit_qlinear_ws -- orbit_qlinear_ex with a caller-owned device workspace.  With
+ * workspace_bytes at least orbit_qlinear_workspace_size(M, N, K) on the same device (and
+ * workspace 16-byte aligned) a small layer runs split over K: the splits' fp32 sums are added in
+ * split order (deterministic for a given device) before the epilogue, so the result differs from
+ * orbit_qlinear_ex's only in the fp32 rounding of the sum over K.  Otherwise (a NULL or too small
+ * workspace, or a layer that does not split) it is orbit_qlinear_ex.  The library does not keep
+ * the pointer; the caller keeps the workspace alive and unused by other work until the call's
+ * work on `stream` has finished, and gives concurrent calls separate workspaces.
+ *   other arguments, limits and errors as for orbit_qlinear_ex.
+ */
+orbit_status orbit_qlinear_ws(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                              orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
+                              int64_t K, const uint16_t* bias, int32_t act, int32_t out_dtype, void* Y,
+                              int64_t ldy, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * adaln_int4_quantize_weights -- the offline pass of the adjacent layer type: the adaptive-layer-
  * norm modulation projections, which the paper keeps at INT4 weight round-to-nearest with group
  * size 64 and BF16 activations, unrotated (Sec. 5 setup; supplementary layer list; Sec. 6.2

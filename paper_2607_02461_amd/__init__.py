@@ -46,6 +46,10 @@ SIGNATURES = {
     "orbit_qlinear_ex": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
                                         _c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _c_void_p, _i64,
                                         _c_void_p]),
+    "orbit_qlinear_workspace_size": (ctypes.c_int, [_i64, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "orbit_qlinear_ws": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
+                                        _c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _c_void_p, _i64,
+                                        _c_void_p, ctypes.c_size_t, _c_void_p]),
     "adaln_int4_quantize_weights": (ctypes.c_int, [_c_void_p, _i64, _i64, _i64, _c_void_p, _c_void_p, _c_void_p]),
     "adaln_int4_linear": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _i64, _i64, _c_void_p,
                                          _c_void_p, _i64, _c_void_p]),
@@ -294,6 +298,41 @@ def orbit_qlinear_ex(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor
     return out
 
 
+def orbit_qlinear_workspace_size(M: int, N: int, K: int, device=None) -> int:
+    """Bytes of workspace with which orbit_qlinear_ws splits an M x N x K layer over K on
+    `device` (default: the current one); 0 when it would not split."""
+    n = ctypes.c_size_t(0)
+    with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
+        _check("orbit_qlinear_workspace_size", lib().orbit_qlinear_workspace_size(M, N, K, ctypes.byref(n)))
+    return n.value
+
+
+def orbit_qlinear_ws(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor, cb_w: Codebook,
+                     w_codes: torch.Tensor, w_norm: torch.Tensor, workspace: torch.Tensor, bias: torch.Tensor = None,
+                     gelu: bool = False, out_dtype: torch.dtype = torch.float32,
+                     out: torch.Tensor = None) -> torch.Tensor:
+    """orbit_qlinear_ex with a caller workspace (a contiguous device tensor of any dtype, at least
+    orbit_qlinear_workspace_size bytes, used on the current stream) that lets a small layer split
+    over K."""
+    M, N, K, dev = _qlinear_operands(cb_a, x_codes, x_norm, cb_w, w_codes, w_norm)
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
+    if not isinstance(workspace, torch.Tensor) or workspace.device != dev or not workspace.is_contiguous():
+        raise ValueError(f"workspace must be a contiguous tensor on {dev}")
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype, device=dev)
+    _check_out(out, M, N, out_dtype, dev)
+    if bias is not None:
+        _expect(bias, "bias", torch.bfloat16, (N,), dev)
+    with torch.cuda.device(dev):
+        _check("orbit_qlinear_ws", lib().orbit_qlinear_ws(
+            cb_a.handle, _ptr(x_codes), _ptr(x_norm), M, cb_w.handle, _ptr(w_codes), _ptr(w_norm), N, K,
+            _ptr(bias) if bias is not None else None, ORBIT_ACT_GELU if gelu else ORBIT_ACT_NONE,
+            ORBIT_OUT_BF16 if out_dtype == torch.bfloat16 else ORBIT_OUT_F32, _ptr(out), max(out.stride(0), N),
+            _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(x_codes)))
+    return out
+
+
 def adaln_int4_quantize_weights(W: torch.Tensor, q: torch.Tensor = None, scales: torch.Tensor = None):
     """Offline INT4 round-to-nearest of an AdaLN modulation projection (group 64): returns
     (q uint8 [N, K/2] with code + 8 per nibble, scales fp16 [N, K/64])."""
@@ -334,5 +373,6 @@ def adaln_int4_linear(X: torch.Tensor, q: torch.Tensor, scales: torch.Tensor, bi
 
 
 __all__ = ["adaln_int4_quantize_weights", "adaln_int4_linear", "rpbh_plan", "rpbh_plan_from_arrays", "lloydmax_codebook", "quantize_weights_offline",
-           "rpbh_quantize_act", "orbit_qlinear", "orbit_qlinear_ex", "Plan", "Codebook", "OrbitError", "lib", "LIB_PATH",
+           "rpbh_quantize_act", "orbit_qlinear", "orbit_qlinear_ex",
+           "orbit_qlinear_workspace_size", "orbit_qlinear_ws", "Plan", "Codebook", "OrbitError", "lib", "LIB_PATH",
            "SIGNATURES", "code_bytes"]

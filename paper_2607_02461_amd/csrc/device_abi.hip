@@ -206,10 +206,10 @@ orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t
     return quantize_rows("rpbh_quantize_act", p, cb_a, X, M, K, ldx, eps, x_codes, x_norm, false, stream);
 }
 
-orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+orbit_status orbit_qlinear_ws(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
                               orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
                               int64_t K, const uint16_t* bias, int32_t act, int32_t out_dtype, void* Y, int64_t ldy,
-                              void* stream) {
+                              void* workspace, size_t workspace_bytes, void* stream) {
     clear_error();
     if (!cb_a || !cb_w) return fail(ORBIT_EINVAL, "orbit_qlinear: codebook is NULL");
     if (M < 0 || N < 0) return fail(ORBIT_EINVAL, "orbit_qlinear: negative M or N");
@@ -253,6 +253,13 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
     g.gelu = act == ORBIT_ACT_GELU;
     g.out_bf16 = out_dtype == ORBIT_OUT_BF16;
     g.vec4 = aligned(Y, 4 * ysize) && ldy % 4 == 0 && aligned(w_norm, 8) && (!bias || aligned(bias, 8));
+    // K-split of a small grid, when the caller's workspace holds the partial sums
+    g.splits = lut_gemm_splits(M, N, K, info.cus, &g.split_steps);
+    if (g.splits > 1 && workspace && aligned(workspace, 16) &&
+        workspace_bytes >= (size_t)g.splits * (size_t)M * (size_t)N * sizeof(float))
+        g.ws = (float*)workspace;
+    else
+        g.splits = 1;
     for (const orbit_codebook_s* cb : {cb_a, cb_w}) {
         // the 4-bit decoder reads the positive half and mirrors it
         if (cb->bits != 4) continue;
@@ -329,6 +336,32 @@ orbit_status orbit_qlinear(orbit_codebook cb_a, const uint8_t* x_codes, const fl
                            float* Y, int64_t ldy, void* stream) {
     return orbit_qlinear_ex(cb_a, x_codes, x_norm, M, cb_w, w_codes, w_norm, N, K, nullptr, ORBIT_ACT_NONE,
                             ORBIT_OUT_F32, Y, ldy, stream);
+}
+
+orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                              orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
+                              int64_t K, const uint16_t* bias, int32_t act, int32_t out_dtype, void* Y, int64_t ldy,
+                              void* stream) {
+    return orbit_qlinear_ws(cb_a, x_codes, x_norm, M, cb_w, w_codes, w_norm, N, K, bias, act, out_dtype, Y, ldy,
+                            nullptr, 0, stream);
+}
+
+orbit_status orbit_qlinear_workspace_size(int64_t M, int64_t N, int64_t K, size_t* bytes) {
+    clear_error();
+    if (!bytes) return fail(ORBIT_EINVAL, "orbit_qlinear_workspace_size: null output pointer");
+    *bytes = 0;
+    if (M < 0 || N < 0) return fail(ORBIT_EINVAL, "orbit_qlinear_workspace_size: negative M or N");
+    if (K <= 0 || K % 64 != 0 || K > (int64_t)1 << 30)
+        return fail(ORBIT_EINVAL, "orbit_qlinear_workspace_size: K=%lld must be a positive multiple of 64", (long long)K);
+    if (M == 0 || N == 0) return ORBIT_OK;
+    int dev;
+    DeviceInfo info;
+    orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    int steps = 0;
+    const int splits = lut_gemm_splits(M, N, K, info.cus, &steps);
+    if (splits > 1) *bytes = (size_t)splits * (size_t)M * (size_t)N * sizeof(float);
+    return ORBIT_OK;
 }
 
 }  // extern "C"

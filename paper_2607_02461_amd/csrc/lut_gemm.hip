@@ -12,6 +12,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "device.h"
 
 namespace orbit {
@@ -215,7 +217,9 @@ __device__ __forceinline__ void store_one(const GemmParams& p, int64_t row, int6
         ((float*)p.Y)[row * p.ldy + col] = v;
 }
 
-template <int BA, int BW>
+// SPLIT: workgroup z of a K-split contracts K-steps z*steps .. (z+1)*steps - 1 (the last split
+// fewer) and stores its raw sums to p.ws[z][M][N]; lut_gemm_reduce applies the epilogue.
+template <int BA, int BW, bool SPLIT>
 __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     __shared__ __align__(16) _Float16 As[BM * LDS_STRIDE];
     __shared__ __align__(16) _Float16 Bs[BN * LDS_STRIDE];
@@ -234,8 +238,11 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     const int lr = tid >> 1, lh = tid & 1;
     const int64_t arow = min(m0 + lr, p.M - 1), brow = min(n0 + lr, p.N - 1);
     const int64_t a_row_bytes = (int64_t)p.K * BA / 8, b_row_bytes = (int64_t)p.K * BW / 8;
-    const uint8_t* asrc = p.xc + arow * a_row_bytes + lh * 4 * BA;
-    const uint8_t* bsrc = p.wc + brow * b_row_bytes + lh * 4 * BW;
+    // the K-steps this workgroup contracts
+    const int kb = SPLIT ? (int)blockIdx.z * p.split_steps : 0;
+    const int nk = SPLIT ? min(p.split_steps, p.K / BK - kb) : p.K / BK;
+    const uint8_t* asrc = p.xc + arow * a_row_bytes + lh * 4 * BA + (int64_t)kb * (BK * BA / 8);
+    const uint8_t* bsrc = p.wc + brow * b_row_bytes + lh * 4 * BW + (int64_t)kb * (BK * BW / 8);
 
     floatx16 acc[2][2];
 #pragma unroll
@@ -249,7 +256,6 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     // small grids each workgroup's time is its chain of K-steps, which would otherwise wait for
     // one global load per step.  The ring is unrolled so that every slot is a fixed register set.
     constexpr int D = 4;  // the ring's slots (unrolled below)
-    const int nk = p.K / BK;
     const int64_t astep = BK * BA / 8, bstep = BK * BW / 8;
     Codes<BA> ca[D];
     Codes<BW> cb[D];
@@ -308,6 +314,22 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     if (s + 2 < nk) step(s + 2, ca[2], cb[2]);
 
     // epilogue: acc element e of a 32x32 tile sits at row 8*(e/4) + 4*(lane/32) + e%4, col lane%32
+    if constexpr (SPLIT) {
+        float* const ws = p.ws + (int64_t)blockIdx.z * p.M * p.N;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
+                if (col >= p.N) continue;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int64_t row = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+                    if (row < p.M) ws[row * p.N + col] = acc[i][j][e];
+                }
+            }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
 #pragma unroll
@@ -576,10 +598,44 @@ hipError_t launch_big(const GemmParams& p, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// The K-splits' sums in split order (deterministic), rescaled and through the layer epilogue:
+// one thread per four consecutive outputs of a row.
+__global__ __launch_bounds__(256) void lut_gemm_reduce(GemmParams p, int splits) {
+    const int64_t nq = (p.N + 3) / 4;
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= p.M * nq) return;
+    const int64_t row = t / nq, c0 = (t - row * nq) * 4;
+    const float xs = p.xn[row];
+    const int nc = (int)min((int64_t)4, p.N - c0);
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int z = 0; z < splits; ++z) {
+        const float* src = p.ws + (int64_t)z * p.M * p.N + row * p.N + c0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            if (r < nc) v[r] += src[r];
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        if (r >= nc) continue;
+        const int64_t col = c0 + r;
+        const float out = epilogue_value(p, v[r] * xs * bf16_to_f32(p.wn[col]), p.bias ? bf16_to_f32(p.bias[col]) : 0.f);
+        store_one(p, row, col, out);
+    }
+}
+
 template <int BA, int BW>
 hipError_t launch_small(const GemmParams& p, hipStream_t stream) {
     dim3 grid((unsigned)((p.N + BN - 1) / BN), (unsigned)((p.M + BM - 1) / BM));
-    hipLaunchKernelGGL((lut_gemm_kernel<BA, BW>), grid, dim3(256), 0, stream, p);
+    if (p.ws && p.splits > 1) {
+        grid.z = (unsigned)p.splits;
+        hipLaunchKernelGGL((lut_gemm_kernel<BA, BW, true>), grid, dim3(256), 0, stream, p);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int64_t threads = p.M * ((p.N + 3) / 4);
+        hipLaunchKernelGGL(lut_gemm_reduce, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p, p.splits);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((lut_gemm_kernel<BA, BW, false>), grid, dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 
@@ -624,6 +680,35 @@ hipError_t launch_one(const GemmParams& p, hipStream_t stream, int cus) {
 }
 
 }  // namespace
+
+int lut_gemm_splits(int64_t M, int64_t N, int64_t K, int cus, int* split_steps) {
+    const int nk = (int)(K / BK);
+    *split_steps = nk;
+    if (((M + BM2 - 1) / BM2) * ((N + BN2 - 1) / BN2) >= cus) return 1;  // the large kernel
+    // A small grid of 128x128 workgroups, each one K-step chain that is latency-bound.  The count
+    // of splits minimises an estimate of the busiest compute unit's time, in K-steps: k co-resident
+    // workgroups of `steps` K-steps take w(k) * steps (measured on 256 compute units: 1, 1.66 and
+    // 2.58 for k = 1, 2, 3, then about 0.86 k), plus the partial sums' round trip through the
+    // workspace at about 7 MB per K-step's time.  At least 4 K-steps per split, at most 64 splits.
+    const int64_t wgs = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    auto busiest = [&](int splits, int steps) {
+        const int64_t k = (wgs * splits + cus - 1) / cus;
+        return (k == 1 ? 1.0 : k == 2 ? 1.66 : k == 3 ? 2.58 : 0.86 * (double)k) * steps;
+    };
+    int best_splits = 1, best_steps = nk;
+    double best = busiest(1, nk);
+    for (int s = 2; s <= std::min(64, nk / 4); ++s) {
+        const int steps = (nk + s - 1) / s, splits = (nk + steps - 1) / steps;
+        const double cost = busiest(splits, steps) + (double)splits * (double)M * (double)N * 8.0 / 7.0e6;
+        if (cost < best) {
+            best = cost;
+            best_splits = splits;
+            best_steps = steps;
+        }
+    }
+    *split_steps = best_steps;
+    return best_splits;
+}
 
 hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, int cus, hipStream_t stream) {
     switch (ba * 8 + bw) {

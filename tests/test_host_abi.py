@@ -162,6 +162,36 @@ def test_device_calls_validate_before_launch():
     assert lib.orbit_last_error().decode() == ""
 
 
+def test_qlinear_workspace_calls_validate_before_launch():
+    lib = oq.lib()
+    cb4, cb_other = oq.lloydmax_codebook(4, 256), oq.lloydmax_codebook(4, 512)
+    null = ctypes.c_void_p(0)
+    fake = ctypes.c_void_p(1 << 20)
+    n = ctypes.c_size_t(7)
+    # the size query: argument errors before any device is asked; an empty layer needs nothing
+    st, _ = _status(lib.orbit_qlinear_workspace_size, 4, 4, 256, None)
+    assert st == oq.ORBIT_EINVAL
+    for M, N, K in ((-1, 4, 256), (4, -1, 256), (4, 4, 0), (4, 4, 100), (4, 4, (1 << 30) + 64)):
+        st, _ = _status(lib.orbit_qlinear_workspace_size, M, N, K, ctypes.byref(n))
+        assert st == oq.ORBIT_EINVAL and n.value == 0
+    for M, N in ((0, 3072), (256, 0)):
+        n.value = 7
+        st, _ = _status(lib.orbit_qlinear_workspace_size, M, N, 3072, ctypes.byref(n))
+        assert st == oq.ORBIT_OK and n.value == 0
+    # the layer with a workspace validates as orbit_qlinear_ex does
+    ws = ctypes.c_size_t(1 << 20)
+    st, _ = _status(lib.orbit_qlinear_ws, cb4.handle, fake, fake, 4, cb_other.handle, fake, fake, 4, 256, null,
+                    0, 0, fake, 4, fake, ws, null)
+    assert st == oq.ORBIT_EINVAL
+    st, _ = _status(lib.orbit_qlinear_ws, cb4.handle, fake, fake, 4, cb4.handle, fake, fake, 4, 256, null,
+                    2, 0, fake, 4, fake, ws, null)
+    assert st == oq.ORBIT_EINVAL   # unknown act
+    st, _ = _status(lib.orbit_qlinear_ws, cb4.handle, null, null, 0, cb4.handle, null, null, 4, 256, null,
+                    0, 0, null, 4, null, ctypes.c_size_t(0), null)
+    assert st == oq.ORBIT_OK
+    assert lib.orbit_last_error().decode() == ""
+
+
 def test_device_calls_reject_grids_beyond_32_bits():
     lib = oq.lib()
     p = oq.rpbh_plan(256, 128, 0)
