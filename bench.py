@@ -107,7 +107,7 @@ def main():
         xc = torch.empty((lin.M, lin.K * lin.ba // 8), dtype=torch.uint8, device=dev)
         xn = torch.empty((lin.M,), dtype=torch.float32, device=dev)
         Y = torch.empty((lin.M, lin.N), dtype=torch.float32, device=dev)
-        # the K-split workspace of a layer too small to fill the GPU (none for c4's projections)
+        # the K-split workspace of the rows the 128x128 kernel runs (c1: all; c4 down: its last 504)
         wsp = torch.empty(max(16, oq.orbit_qlinear_workspace_size(lin.M, lin.N, lin.K)), dtype=torch.uint8,
                           device=dev)
         layers.append(dict(lin=lin, X=X, W=W, wc=wc, wn=wn, xc=xc, xn=xn, Y=Y, ws=wsp,
@@ -193,7 +193,9 @@ def main():
     roofline = {
         "kernel": "lut_gemm_big" if wl is workloads.C4 else (
             "lut_gemm_kernel+lut_gemm_reduce" if layers[0]["ws"].numel() > 16 else "lut_gemm_kernel"),
-        "k_splits": [L["ws"].numel() // (4 * L["lin"].M * L["lin"].N) or 1 for L in layers],
+        # c4's down-projection: lut_gemm_big on the rows of its full rounds, then the other rows
+        # on the 128x128 kernel split over K (the workspace) and lut_gemm_reduce
+        "workspace_bytes": [oq.orbit_qlinear_workspace_size(L["lin"].M, L["lin"].N, L["lin"].K) for L in layers],
         "bound": "mfma",
         "achieved": gemm_launch_flops / (gemm_avg_ms * 1e-3) / 1e12,
         "peak": FP16_MFMA_PEAK_TFLOPS,
@@ -324,17 +326,17 @@ def main():
 
         def chain_fused():
             oq.rpbh_quantize_act(L0["plan"], L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
-            oq.orbit_qlinear_ex(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], gelu=True,
+            oq.orbit_qlinear_ws(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["ws"], gelu=True,
                                 out_dtype=torch.bfloat16, out=H)
             oq.rpbh_quantize_act(L1["plan"], L1["cba"], H, 1e-10, L1["xc"], L1["xn"])
-            oq.orbit_qlinear(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["Y"])
+            oq.orbit_qlinear_ws(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["ws"], out=L1["Y"])
 
         def chain_unfused():
             oq.rpbh_quantize_act(L0["plan"], L0["cba"], L0["X"], 1e-10, L0["xc"], L0["xn"])
-            oq.orbit_qlinear(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"])
+            oq.orbit_qlinear_ws(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["ws"], out=L0["Y"])
             H.copy_(torch.nn.functional.gelu(L0["Y"]))
             oq.rpbh_quantize_act(L1["plan"], L1["cba"], H, 1e-10, L1["xc"], L1["xn"])
-            oq.orbit_qlinear(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["Y"])
+            oq.orbit_qlinear_ws(L1["cba"], L1["xc"], L1["xn"], L1["cbw"], L1["wc"], L1["wn"], L1["ws"], out=L1["Y"])
 
         chain = {"layers": f"{L0['lin'].name} -> GELU -> {L1['lin'].name}"}
         for name, fn in (("fused_ms", chain_fused), ("unfused_ms", chain_unfused)):

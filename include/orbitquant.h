@@ -228,11 +228,11 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
 /*
  * orbit_qlinear_workspace_size -- bytes of device workspace with which orbit_qlinear_ws splits
  * the contraction over K for a layer of M x N outputs and K inputs on the current device; 0 when
- * it would not split (a layer that already fills the device's compute units, or too short a K).
- * A split is worth it where the grid of output tiles is small (few tokens, Sec. 5's low-batch
- * serving): each split contracts a contiguous range of K, so one layer keeps every compute unit busy.
+ * it would not split.  A split pays where the grid of output tiles is too small to fill the
+ * device: a layer of few tokens, or the rows of a large layer's last, partly filled round of
+ * tiles.  Each split contracts a contiguous range of K, so every compute unit stays busy.
  *
- *   bytes  host, out: splits * M * N * 4 (fp32 partial sums), or 0
+ *   bytes  host, out: splits * (rows split) * N * 4 (fp32 partial sums), or 0
  *
  * Errors: ORBIT_EINVAL (null bytes, negative M or N, K not a positive multiple of 64 up to
  * 2^30); ORBIT_EHIP (no device).  M = 0 or N = 0 gives 0.
@@ -242,7 +242,7 @@ orbit_status orbit_qlinear_workspace_size(int64_t M, int64_t N, int64_t K, size_
 /*
  * orbit_qlinear_ws -- orbit_qlinear_ex with a caller-owned device workspace.  With
  * workspace_bytes at least orbit_qlinear_workspace_size(M, N, K) on the same device (and
- * workspace 16-byte aligned) a small layer runs split over K: the splits' fp32 sums are added in
+ * workspace 16-byte aligned) the rows of a small grid run split over K: the splits' fp32 sums are added in
  * split order (deterministic for a given device) before the epilogue, so the result differs from
  * orbit_qlinear_ex's only in the fp32 rounding of the sum over K.  Otherwise (a NULL or too small
  * workspace, or a layer that does not split) it is orbit_qlinear_ex.  The library does not keep

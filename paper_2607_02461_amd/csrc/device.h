@@ -70,15 +70,18 @@ struct GemmParams {
     int out_bf16;          // store Y as bf16 (round to nearest even) instead of fp32
     uint16_t lut_a[64];    // fp16 levels (2^ba used)
     uint16_t lut_w[16];    // fp16 levels (2^bw used)
-    // K-split of a small grid (caller workspace): fp32 partial sums [splits][M][N], each split
-    // split_steps K-steps of 64; ws = null runs unsplit
+    // K-split of the 128x128 kernel's rows (caller workspace): fp32 partial sums [splits][M][N]
+    // of the rows it runs, each split split_steps K-steps of 64; ws = null runs unsplit
     float* ws;
     int splits, split_steps;
 };
 
 hipError_t launch_lut_gemm(const GemmParams& p, int ba, int bw, int cus, hipStream_t stream);
-// K-splits a layer of this shape uses on `cus` compute units (1: none), and the steps per split
-int lut_gemm_splits(int64_t M, int64_t N, int64_t K, int cus, int* split_steps);
+// Rows [0, m_big) of an M x N layer run on the 256x256 kernel, the rest on the 128x128 kernel
+int64_t lut_gemm_big_rows(int64_t M, int64_t N, int cus);
+// K-splits of the 128x128 kernel on M x N outputs when a workspace is given (1: none), and the
+// K-steps per split (the last split may have fewer)
+int lut_gemm_small_splits(int64_t M, int64_t N, int64_t K, int cus, int* split_steps);
 
 // INT4 round-to-nearest (group 64) weight-only layer of the AdaLN modulation projections.
 struct RtnLinearParams {

@@ -253,10 +253,11 @@ orbit_status orbit_qlinear_ws(orbit_codebook cb_a, const uint8_t* x_codes, const
     g.gelu = act == ORBIT_ACT_GELU;
     g.out_bf16 = out_dtype == ORBIT_OUT_BF16;
     g.vec4 = aligned(Y, 4 * ysize) && ldy % 4 == 0 && aligned(w_norm, 8) && (!bias || aligned(bias, 8));
-    // K-split of a small grid, when the caller's workspace holds the partial sums
-    g.splits = lut_gemm_splits(M, N, K, info.cus, &g.split_steps);
+    // K-split of the rows the 128x128 kernel runs, when the caller's workspace holds the partial sums
+    const int64_t m_small = M - lut_gemm_big_rows(M, N, info.cus);
+    g.splits = m_small > 0 ? lut_gemm_small_splits(m_small, N, K, info.cus, &g.split_steps) : 1;
     if (g.splits > 1 && workspace && aligned(workspace, 16) &&
-        workspace_bytes >= (size_t)g.splits * (size_t)M * (size_t)N * sizeof(float))
+        workspace_bytes >= (size_t)g.splits * (size_t)m_small * (size_t)N * sizeof(float))
         g.ws = (float*)workspace;
     else
         g.splits = 1;
@@ -358,9 +359,10 @@ orbit_status orbit_qlinear_workspace_size(int64_t M, int64_t N, int64_t K, size_
     DeviceInfo info;
     orbit_status st = current_device(&dev, &info);
     if (st != ORBIT_OK) return st;
+    const int64_t m_small = M - lut_gemm_big_rows(M, N, info.cus);
     int steps = 0;
-    const int splits = lut_gemm_splits(M, N, K, info.cus, &steps);
-    if (splits > 1) *bytes = (size_t)splits * (size_t)M * (size_t)N * sizeof(float);
+    const int splits = m_small > 0 ? lut_gemm_small_splits(m_small, N, K, info.cus, &steps) : 1;
+    if (splits > 1) *bytes = (size_t)splits * (size_t)m_small * (size_t)N * sizeof(float);
     return ORBIT_OK;
 }
 

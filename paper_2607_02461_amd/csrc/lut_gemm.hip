@@ -651,10 +651,23 @@ inline GemmParams rows_from(const GemmParams& p, int64_t m0, int ba) {
 
 template <int BA, int BW>
 hipError_t launch_one(const GemmParams& p, hipStream_t stream, int cus) {
+    const int64_t m_big = lut_gemm_big_rows(p.M, p.N, cus);
+    if (m_big == 0) return launch_small<BA, BW>(p, stream);
+    if (m_big == p.M) return launch_big<BA, BW>(p, stream);
+    GemmParams head = p;
+    head.M = m_big;
+    hipError_t e = launch_big<BA, BW>(head, stream);
+    if (e != hipSuccess) return e;
+    return launch_small<BA, BW>(rows_from(p, m_big, BA), stream);
+}
+
+}  // namespace
+
+int64_t lut_gemm_big_rows(int64_t M, int64_t N, int cus) {
     // the large kernel from one 256x256 tile per compute unit up (measured: at 432 tiles on 256
     // compute units it beats the 128x128 kernel by a quarter, despite its half-empty second round)
-    const int64_t ntm = (p.M + BM2 - 1) / BM2, ntn = (p.N + BN2 - 1) / BN2, tiles = ntm * ntn;
-    if (tiles < (int64_t)cus) return launch_small<BA, BW>(p, stream);
+    const int64_t ntm = (M + BM2 - 1) / BM2, ntn = (N + BN2 - 1) / BN2, tiles = ntm * ntn;
+    if (tiles < (int64_t)cus) return 0;
     // Wave quantization: the large kernel runs one tile per compute unit at a time, so a last round
     // that is only partly full costs as long as a full one (c4's down-projection: 2600 tiles, an
     // eleventh round of 40).  When that pays, the large kernel takes the tile rows that fill its
@@ -665,28 +678,19 @@ hipError_t launch_one(const GemmParams& p, hipStream_t stream, int cus) {
     const int64_t rows_big = (tiles / cus) * cus / ntn;
     if (rows_big > 0 && rows_big < ntm) {
         const int64_t m0 = rows_big * BM2;
-        const int64_t small_wgs = ((p.M - m0 + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+        const int64_t small_wgs = ((M - m0 + BM - 1) / BM) * ((N + BN - 1) / BN);
         const double whole = (double)((tiles + cus - 1) / cus);
         const double split = (double)((rows_big * ntn + cus - 1) / cus) + 0.6 * (double)((small_wgs + cus - 1) / cus);
-        if (split + 0.1 < whole) {
-            GemmParams head = p;
-            head.M = m0;
-            hipError_t e = launch_big<BA, BW>(head, stream);
-            if (e != hipSuccess) return e;
-            return launch_small<BA, BW>(rows_from(p, m0, BA), stream);
-        }
+        if (split + 0.1 < whole) return m0;
     }
-    return launch_big<BA, BW>(p, stream);
+    return M;
 }
 
-}  // namespace
-
-int lut_gemm_splits(int64_t M, int64_t N, int64_t K, int cus, int* split_steps) {
+int lut_gemm_small_splits(int64_t M, int64_t N, int64_t K, int cus, int* split_steps) {
     const int nk = (int)(K / BK);
     *split_steps = nk;
-    if (((M + BM2 - 1) / BM2) * ((N + BN2 - 1) / BN2) >= cus) return 1;  // the large kernel
-    // A small grid of 128x128 workgroups, each one K-step chain that is latency-bound.  The count
-    // of splits minimises an estimate of the busiest compute unit's time, in K-steps: k co-resident
+    // The 128x128 workgroups are each one K-step chain that is latency-bound.  The count of splits
+    // minimises an estimate of the busiest compute unit's time, in K-steps: k co-resident
     // workgroups of `steps` K-steps take w(k) * steps (measured on 256 compute units: 1, 1.66 and
     // 2.58 for k = 1, 2, 3, then about 0.86 k), plus the partial sums' round trip through the
     // workspace at about 7 MB per K-step's time.  At least 4 K-steps per split, at most 64 splits.

@@ -64,6 +64,31 @@ def test_split_matches_oracle_and_unsplit(M, N, K, ba, bw):
     assert d <= 1e-5
 
 
+# Grids of a large tile per compute unit or more whose last round of large tiles would be mostly
+# empty: the large kernel takes the rows of its full rounds and the 128x128 kernel the rest (37
+# and 517 rows on 256 compute units), split over K with the workspace.  Sampled rows from both
+# parts against the oracle, every output against the unsplit layer.
+@pytest.mark.parametrize("M,N,K", [(4133, 8061, 1024), (8197, 4099, 4096)])
+def test_split_tail_of_large_grid(M, N, K):
+    ba, bw = 4, 3
+    host, (cba, cbw), (xp, xs, wp, wr) = _operands(M, N, K, ba, bw, seed=M + K)
+    n, ws = _workspace(M, N, K)
+    assert 0 < n < M * N * 4            # partial sums for the tail rows only
+    Y = oq.orbit_qlinear_ws(cba, xp, xs, cbw, wp, wr, ws)
+    Y0 = oq.orbit_qlinear(cba, xp, xs, cbw, wp, wr)
+    torch.cuda.synchronize()
+    Y, Y0 = Y.cpu().numpy().astype(np.float64), Y0.cpu().numpy().astype(np.float64)
+    rows = np.unique(np.concatenate([np.random.default_rng(K).choice(M, 48, replace=False),
+                                     np.arange(M - 16, M)]))
+    xc, xsh, wc, wrh = host
+    ref = qlinear_oracle_fp16(xc.numpy()[rows], xsh.double().numpy()[rows], ba, wc.numpy(), wrh.double().numpy(),
+                              bw, K)
+    err, d = rel_frobenius(Y[rows], ref), rel_frobenius(Y, Y0)
+    log_stats(f"split tail M={M} N={N} K={K} workspace={n}", rel_f=err, vs_unsplit=d)
+    assert err <= GEMM_REL_F
+    assert d <= 1e-5
+
+
 @pytest.mark.parametrize("bias,gelu,bf16", [(True, False, False), (False, True, False), (False, False, True),
                                             (True, True, True)])
 @pytest.mark.parametrize("pad", [0, 1])
