@@ -1,8 +1,8 @@
 """Streams and graph capture through the C ABI: device calls only enqueue on the caller's stream,
 handles may be shared by calls on several streams at once, and once a plan and codebook have been
-used on the device (their tables uploaded), the quantizer and the layer can be captured in a HIP
-graph and replayed.  Every kernel is deterministic, so each result is compared bit for bit with the
-same call made eagerly on the default stream."""
+used on the device (their tables uploaded), the quantizer and the layer (also split over K with a
+workspace) can be captured in a HIP graph and replayed.  Every kernel is deterministic, so each
+result is compared bit for bit with the same call made eagerly on the default stream."""
 
 import numpy as np
 import pytest
@@ -86,6 +86,49 @@ def test_graph_capture_and_replay():
         got = (xc.clone(), xn.clone(), Y.clone())
         _ = _bf16(1024, 1024, 7).float().sum()       # unrelated eager work between replays
         step()                                        # the same step, eagerly
+        torch.cuda.synchronize()
+        for a, b, name in zip(got, (xc, xn, Y), ("codes", "norms", "Y")):
+            assert torch.equal(a, b), f"replay {r}: {name} differ from the eager step"
+
+
+def test_graph_capture_of_split_layer():
+    # c1's layer split over K with a workspace (two kernels, no memset) captured with its
+    # quantizer, replayed on new inputs; every replay equals the eager step
+    K, M, N = 3072, 256, 3072
+    plan, cb = oq.rpbh_plan(K, 128, 0), oq.lloydmax_codebook(4, K)
+    W = _bf16(N, K, 19, scale=0.02)
+    wc, wn = oq.quantize_weights_offline(plan, cb, W)
+    bias = (torch.randn(N, device=DEV) * 0.1).to(torch.bfloat16)
+    X = _bf16(M, K, 20)
+    xc = torch.empty((M, K // 2), dtype=torch.uint8, device=DEV)
+    xn = torch.empty((M,), dtype=torch.float32, device=DEV)
+    Y = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+    n = oq.orbit_qlinear_workspace_size(M, N, K)
+    assert n > 0
+    ws = torch.empty(n, dtype=torch.uint8, device=DEV)
+
+    def step():
+        oq.rpbh_quantize_act(plan, cb, X, 1e-10, xc, xn)
+        oq.orbit_qlinear_ws(cb, xc, xn, cb, wc, wn, ws, bias=bias, gelu=True, out_dtype=torch.bfloat16, out=Y)
+
+    step()
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    for r in range(4):
+        X.copy_(_bf16(M, K, 200 + r, scale=1.0 + r))
+        g.replay()
+        torch.cuda.synchronize()
+        got = (xc.clone(), xn.clone(), Y.clone())
+        ws.fill_(255)                                 # stale workspace between replays
+        step()
         torch.cuda.synchronize()
         for a, b, name in zip(got, (xc, xn, Y), ("codes", "norms", "Y")):
             assert torch.equal(a, b), f"replay {r}: {name} differ from the eager step"
