@@ -606,6 +606,34 @@ __global__ __launch_bounds__(256) void lut_gemm_reduce(GemmParams p, int splits)
     if (t >= p.M * nq) return;
     const int64_t row = t / nq, c0 = (t - row * nq) * 4;
     const float xs = p.xn[row];
+    if (p.vec4 && (p.N & 3) == 0) {
+        // whole runs of four, 16-byte aligned in the workspace and in Y: vector loads and stores
+        const int64_t plane = p.M * p.N;
+        const float* src = p.ws + row * p.N + c0;
+        float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int z = 0; z < splits; ++z) {
+            const float4 b = *(const float4*)(src + z * plane);
+            a.x += b.x;
+            a.y += b.y;
+            a.z += b.z;
+            a.w += b.w;
+        }
+        const uint2 rw = *(const uint2*)(p.wn + c0);
+        const uint2 bb = p.bias ? *(const uint2*)(p.bias + c0) : make_uint2(0u, 0u);
+        float v[4] = {a.x * xs * __uint_as_float(rw.x << 16), a.y * xs * __uint_as_float(rw.x & 0xFFFF0000u),
+                      a.z * xs * __uint_as_float(rw.y << 16), a.w * xs * __uint_as_float(rw.y & 0xFFFF0000u)};
+        v[0] = epilogue_value(p, v[0], __uint_as_float(bb.x << 16));
+        v[1] = epilogue_value(p, v[1], __uint_as_float(bb.x & 0xFFFF0000u));
+        v[2] = epilogue_value(p, v[2], __uint_as_float(bb.y << 16));
+        v[3] = epilogue_value(p, v[3], __uint_as_float(bb.y & 0xFFFF0000u));
+        if (p.out_bf16)
+            *(uint2*)((uint16_t*)p.Y + row * p.ldy + c0) =
+                make_uint2(f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16),
+                           f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16));
+        else
+            *(float4*)((float*)p.Y + row * p.ldy + c0) = make_float4(v[0], v[1], v[2], v[3]);
+        return;
+    }
     const int nc = (int)min((int64_t)4, p.N - c0);
     float v[4] = {0.f, 0.f, 0.f, 0.f};
     for (int z = 0; z < splits; ++z) {
