@@ -241,13 +241,16 @@ orbit_status orbit_qlinear_workspace_size(int64_t M, int64_t N, int64_t K, size_
 
 /*
  * orbit_qlinear_ws -- orbit_qlinear_ex with a caller-owned device workspace.  With
- * workspace_bytes at least orbit_qlinear_workspace_size(M, N, K) on the same device (and
- * workspace 16-byte aligned) the rows of a small grid run split over K: the splits' fp32 sums are added in
- * split order (deterministic for a given device) before the epilogue, so the result differs from
- * orbit_qlinear_ex's only in the fp32 rounding of the sum over K.  Otherwise (a NULL or too small
- * workspace, or a layer that does not split) it is orbit_qlinear_ex.  The library does not keep
- * the pointer; the caller keeps the workspace alive and unused by other work until the call's
- * work on `stream` has finished, and gives concurrent calls separate workspaces.
+ * workspace_bytes at least orbit_qlinear_workspace_size(M, N, K) on the same device (and the
+ * workspace 16-byte aligned) the rows of a small grid run split over K: the splits' fp32 sums
+ * are added in split order (deterministic for a given device) before the epilogue, so the result
+ * differs from orbit_qlinear_ex's only in the fp32 rounding of the sum over K.  Otherwise (a
+ * NULL or too small workspace, or a layer that does not split) it is orbit_qlinear_ex.  The
+ * workspace's contents on entry do not matter.  The library does not keep the pointer; the
+ * caller keeps the workspace alive and unused by other work until the call's work on `stream`
+ * has finished, and gives concurrent calls separate workspaces.
+ *   workspace        device, or NULL
+ *   workspace_bytes  its size in bytes
  *   other arguments, limits and errors as for orbit_qlinear_ex.
  */
 orbit_status orbit_qlinear_ws(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
