@@ -132,3 +132,31 @@ def test_graph_capture_of_split_layer():
         torch.cuda.synchronize()
         for a, b, name in zip(got, (xc, xn, Y), ("codes", "norms", "Y")):
             assert torch.equal(a, b), f"replay {r}: {name} differ from the eager step"
+
+
+def test_split_layers_on_two_streams_with_their_own_workspaces():
+    # two small layers split over K run at once on two streams, each with its own workspace,
+    # against the same calls one after the other on the default stream
+    K = 3072
+    plan, cb = oq.rpbh_plan(K, 128, 0), oq.lloydmax_codebook(4, K)
+    shapes = [(256, 3072), (64, 2000)]
+    ops = []
+    for i, (M, N) in enumerate(shapes):
+        xc, xn = oq.rpbh_quantize_act(plan, cb, _bf16(M, K, 30 + i))
+        wc, wn = oq.quantize_weights_offline(plan, cb, _bf16(N, K, 40 + i, scale=0.02))
+        n = oq.orbit_qlinear_workspace_size(M, N, K)
+        assert n > 0
+        ops.append((xc, xn, wc, wn, torch.empty(n, dtype=torch.uint8, device=DEV)))
+    ref = [oq.orbit_qlinear_ws(cb, xc, xn, cb, wc, wn, ws) for xc, xn, wc, wn, ws in ops]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    out = [None, None]
+    for _ in range(3):
+        for i, (xc, xn, wc, wn, ws) in enumerate(ops):
+            with torch.cuda.stream(streams[i]):
+                out[i] = oq.orbit_qlinear_ws(cb, xc, xn, cb, wc, wn, ws)
+    torch.cuda.synchronize()
+    for i in range(2):
+        assert torch.equal(out[i], ref[i]), f"stream {i}: results differ from the default-stream call"
