@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <algorithm>
 #include <cstring>
 #include <vector>
 
@@ -136,7 +137,9 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
     q.norm = norm;
     q.K = (int)K;
     q.nb = (int)(K / kQuantH);
-    q.R = quant_rows_per_group((int)K);
+    // rows per group: the most a workgroup holds, or fewer when that leaves compute units idle
+    // (a few hundred rows: one row per workgroup spreads them over the device)
+    q.R = (int)std::min<int64_t>(quant_rows_per_group((int)K), (M + info.cus - 1) / info.cus);
     q.ngroups = (int)((M + q.R - 1) / q.R);
     q.eps = eps;
     q.enc = enc;

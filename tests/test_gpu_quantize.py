@@ -32,6 +32,17 @@ def test_small_shapes(K, M, bits, weights):
     compare_quantizer(f"small K={K} M={M}", X, bits, seed=K % 5, weights=weights)
 
 
+# a workgroup holds fewer rows than it could when that leaves compute units idle: ceil(M / 256)
+# rows on 256 compute units, up to 128 / (K / 128).  These row counts step through 1..5 rows per
+# group at K = 3072 (5 at most) and 9 and 20 at K = 256 (64 at most), with ragged last groups.
+@pytest.mark.parametrize("K,M", [(3072, 255), (3072, 257), (3072, 513), (3072, 769), (3072, 1281),
+                                 (256, 2049), (256, 5000)])
+@pytest.mark.parametrize("weights", [False, True])
+def test_rows_per_group_from_row_count(K, M, weights):
+    X = _randn_bf16(M, K, seed=K + 3 * M)
+    compare_quantizer(f"rows per group K={K} M={M}", X, 4, seed=1, weights=weights)
+
+
 # block sizes above 128: the paper's rule (largest power of two dividing d) for the workload
 # dimensions, every size up to 4096 alone, and ragged row counts spanning several groups
 @pytest.mark.parametrize("K,h,M", [(256, 256, 77), (512, 512, 33), (1024, 1024, 129), (2048, 2048, 17),
