@@ -7,6 +7,7 @@ import os
 import re
 
 import numpy as np
+import torch
 import pytest
 
 import oracle
@@ -178,6 +179,11 @@ def test_qlinear_workspace_calls_validate_before_launch():
         n.value = 7
         st, _ = _status(lib.orbit_qlinear_workspace_size, M, N, 3072, ctypes.byref(n))
         assert st == oq.ORBIT_OK and n.value == 0
+    if not torch.cuda.is_available():
+        # a real layer asks the device for its compute units: without one, ORBIT_EHIP and 0 bytes
+        n.value = 7
+        st, msg = _status(lib.orbit_qlinear_workspace_size, 256, 3072, 3072, ctypes.byref(n))
+        assert st == oq.ORBIT_EHIP and n.value == 0 and msg
     # the layer with a workspace validates as orbit_qlinear_ex does
     ws = ctypes.c_size_t(1 << 20)
     st, _ = _status(lib.orbit_qlinear_ws, cb4.handle, fake, fake, 4, cb_other.handle, fake, fake, 4, 256, null,
