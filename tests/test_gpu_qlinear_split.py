@@ -89,6 +89,22 @@ def test_split_tail_of_large_grid(M, N, K):
     assert d <= 1e-5
 
 
+# every bit-width pair the GEMM implements, on c1's layer and a ragged one
+@pytest.mark.parametrize("M,N,K", [(256, 3072, 3072), (33, 200, 2048)])
+@pytest.mark.parametrize("ba,bw", [(3, 3), (3, 2), (2, 3), (2, 4), (4, 2), (6, 3)])
+def test_split_remaining_bit_pairs(M, N, K, ba, bw):
+    host, (cba, cbw), (xp, xs, wp, wr) = _operands(M, N, K, ba, bw, seed=2 * M + N + ba * 8 + bw)
+    n, ws = _workspace(M, N, K)
+    assert _splits(M, N, K, n) >= 2
+    Y = oq.orbit_qlinear_ws(cba, xp, xs, cbw, wp, wr, ws)
+    torch.cuda.synchronize()
+    xc, xsh, wc, wrh = host
+    ref = qlinear_oracle_fp16(xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
+    err = rel_frobenius(Y.cpu().numpy().astype(np.float64), ref)
+    log_stats(f"split bits M={M} N={N} K={K} W{bw}A{ba}", rel_f=err)
+    assert err <= GEMM_REL_F
+
+
 @pytest.mark.parametrize("bias,gelu,bf16", [(True, False, False), (False, True, False), (False, False, True),
                                             (True, True, True)])
 @pytest.mark.parametrize("pad", [0, 1])
