@@ -599,7 +599,7 @@ def adaln_sweep(oq, workloads, dev, steps, warmup=2):
     return out
 
 
-def cpu_baseline(layers, rows):
+def cpu_baseline(layers, rows, min_seconds=10.0):
     """The fp64 oracle timed on the host cores on a bounded sample: `rows` token rows through
     every linear of the step (quantize + contraction).  The oracle's weight codes are made
     once, outside the timing, as the GPU's offline weight pass is outside the step."""
@@ -620,10 +620,10 @@ def cpu_baseline(layers, rows):
         X = L["X"][:rows].float().cpu().numpy().astype(np.float64)
         prepared.append((lin, plan, cba, cbw, cw, r, X))
     # a workload with fewer rows than the sample asks for (c1: 256) repeats its rows, and passes
-    # continue until at least 10 s of work, so that the rate is not a timer artefact
+    # continue until at least min_seconds of work, so that the rate is not a timer artefact
     t0 = time.perf_counter()
     flops, done, passes = 0.0, 0, 0
-    while done < rows or time.perf_counter() - t0 < 10.0:
+    while done < rows or time.perf_counter() - t0 < min_seconds:
         for lin, plan, cba, cbw, cw, r, X in prepared:
             cx, s, _ = oracle.quantize_act(X, plan, cba)
             oracle.qlinear(cx, s, cba.levels, cw, r, cbw.levels)

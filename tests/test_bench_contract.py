@@ -31,3 +31,18 @@ def test_no_gpu_is_reported_not_emulated():
     rc, lines = _run("--steps", "1", "--warmup", "0")
     assert rc == 2 and len(lines) == 1
     assert json.loads(lines[0]) == {"error": "no GPU visible"}
+
+
+def test_cpu_baseline_repeats_a_small_sample():
+    # a workload with fewer rows than the sample asks for repeats them: 16 rows, 40 asked -> 3 passes
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2607_02461_amd.workloads import Linear
+    lin = Linear("tiny", 16, 256, 128, 4, 4)
+    g = torch.Generator()
+    g.manual_seed(0)
+    layers = [dict(lin=lin, X=torch.randn((16, 256), generator=g).to(torch.bfloat16),
+                   W=(torch.randn((128, 256), generator=g) * 0.02).to(torch.bfloat16))]
+    out = bench.cpu_baseline(layers, 40, min_seconds=0.0)
+    assert out["kind"] == "oracle" and out["unit"] == "TFLOP/s" and out["value"] > 0
+    assert "16 token rows" in out["sample"] and "3 passes" in out["sample"]
