@@ -23,11 +23,14 @@
  *     They allocate no device memory for their operands.  Argument checks are synchronous
  *     and happen before any launch; a launch failure returns ORBIT_EHIP with HIP's message.
  *   - Handles are immutable after creation and may be used from several threads and streams
- *     at once.  The first device call that uses a plan on a device uploads the plan's
- *     permutation/sign tables to that device (6 bytes per input, hipMalloc + synchronous copy) and
- *     keeps it until the handle is destroyed.  Destroy a handle only after the work that
- *     uses it has finished.  Make that first call outside stream capture; later calls record
- *     only kernel launches and can be captured in a HIP graph and replayed.
+ *     at once.  A plan's permutation/sign tables (6 bytes per input) and a codebook's encoder
+ *     table (at most 32 KB) live on each device that uses them.  They are copied there at set-up
+ *     (hipMalloc + a synchronous copy): when the handle is created, to the device current on the
+ *     creating thread if a HIP device is visible, and on other devices by rpbh_plan_upload /
+ *     lloydmax_codebook_upload.  Device calls never allocate or copy: on a device without the
+ *     handle's tables they return ORBIT_EINVAL.  So every device call, the first included, records
+ *     only kernel launches and can be captured in a HIP graph and replayed.  The tables stay until
+ *     the handle is destroyed; destroy a handle only after the work that uses it has finished.
  */
 #ifndef ORBITQUANT_H
 #define ORBITQUANT_H
@@ -60,7 +63,7 @@ typedef struct orbit_codebook_s* orbit_codebook;
 
 /*
  * rpbh_plan -- draw the RPBH rotation Pi_d = blkdiag(H_h D_1, ..., H_h D_{d/h}) P_pi
- * (Sec. 4.4, Eq. (9); Alg. 1, offline stage).  Host only; touches no GPU.
+ * (Sec. 4.4, Eq. (9); Alg. 1, offline stage), drawn on the host.
  *
  *   d     input dimension, >= 1
  *   h     Hadamard block size: a power of two dividing d; 0 selects the paper's rule,
@@ -75,18 +78,31 @@ typedef struct orbit_codebook_s* orbit_codebook;
  *
  * Conventions: (P_pi x)_j = x[perm[j]] (a gather) and sign[j] multiplies the j-th
  * post-permutation coordinate; H_h is the Sylvester-ordered Walsh-Hadamard matrix scaled
- * by 1/sqrt(h), so Pi_d is orthogonal.  Errors: ORBIT_EINVAL for d < 1, a bad h or a
- * null `out`; ORBIT_ENOMEM.
+ * by 1/sqrt(h), so Pi_d is orthogonal.  With a HIP device visible, the plan's device tables are
+ * copied to the current device before the call returns (see rpbh_plan_upload); without one the
+ * plan is host-only.  Errors: ORBIT_EINVAL for d < 1, a bad h or a null `out`; ORBIT_ENOMEM;
+ * ORBIT_EHIP when the copy to the device fails.
  */
 orbit_status rpbh_plan(int64_t d, int32_t h, uint64_t seed, orbit_plan* out);
 
 /*
  * rpbh_plan_from_arrays -- the same handle built from a caller-supplied permutation and
  * sign vector (host arrays, copied).  perm must be a permutation of 0..d-1, sign entries
- * must be +1 or -1.  Errors: ORBIT_EINVAL otherwise.
+ * must be +1 or -1.  Set-up and errors otherwise as for rpbh_plan; ORBIT_EINVAL for a bad
+ * perm or sign.
  */
 orbit_status rpbh_plan_from_arrays(int64_t d, int32_t h, const int32_t* perm, const int8_t* sign,
                                    orbit_plan* out);
+
+/*
+ * rpbh_plan_upload -- copy the plan's device tables (gather offsets with the signs folded in, and
+ * the sign masks of the identity-permutation path: 6 bytes per input) to the current device, for
+ * the device calls made there.  Creation already did this for the device current at the time;
+ * another device needs this call once, before its first device call and outside stream capture
+ * (it allocates and copies synchronously).  Repeated calls on a device return ORBIT_OK at once.
+ * Errors: ORBIT_EINVAL (null plan); ORBIT_ENOMEM; ORBIT_EHIP (no device, or a failed copy).
+ */
+orbit_status rpbh_plan_upload(orbit_plan p);
 
 /* Read back a plan.  Any output pointer may be NULL; perm and sign receive d entries. */
 orbit_status rpbh_plan_get(orbit_plan p, int64_t* d, int32_t* h, int32_t* perm, int8_t* sign);
@@ -97,7 +113,7 @@ void rpbh_plan_destroy(orbit_plan p);
 /*
  * lloydmax_codebook -- the Lloyd-Max codebook C^(d,b) for the marginal
  * f_d(t) = Gamma(d/2) / (sqrt(pi) Gamma((d-1)/2)) (1 - t^2)^((d-3)/2) on [-1, 1]
- * (Sec. 3.2, Eqs. (2)-(3); Sec. 4.5; Alg. 1, offline stage).  Host only.
+ * (Sec. 3.2, Eqs. (2)-(3); Sec. 4.5; Alg. 1, offline stage), computed on the host.
  *
  *   bits  1..6 for the codebook itself; the quantizer accepts 2, 3, 4 and 6, the GEMM 2, 3, 4
  *         and 6 for activations and 2..4 for weights
@@ -106,8 +122,10 @@ void rpbh_plan_destroy(orbit_plan p);
  * Computed in fp64 by the fixed-point iteration of the midpoint and centroid conditions on
  * the exact f_d (not its Gaussian approximation).  The levels are exactly antisymmetric
  * and the thresholds are the midpoints of neighbouring levels, so the middle threshold is
- * exactly 0.  Errors: ORBIT_EINVAL for bits or d out of range; ORBIT_EINTERNAL if the
- * iteration fails to converge.
+ * exactly 0.  With a HIP device visible, the encoder table is copied to the current device
+ * before the call returns (see lloydmax_codebook_upload).  Errors: ORBIT_EINVAL for bits or d
+ * out of range; ORBIT_EINTERNAL if the iteration fails to converge; ORBIT_ENOMEM, ORBIT_EHIP
+ * when the copy to the device fails.
  */
 orbit_status lloydmax_codebook(int32_t bits, int64_t d, orbit_codebook* out);
 
@@ -118,6 +136,12 @@ orbit_status lloydmax_codebook(int32_t bits, int64_t d, orbit_codebook* out);
  */
 orbit_status lloydmax_codebook_get(orbit_codebook c, int32_t* bits, int64_t* d, double* levels,
                                    double* thresholds, uint16_t* lut_f16);
+
+/*
+ * lloydmax_codebook_upload -- copy the codebook's encoder table (the quantizer's nearest-level
+ * lookup, at most 8192 fp32 entries) to the current device; as rpbh_plan_upload.
+ */
+orbit_status lloydmax_codebook_upload(orbit_codebook c);
 
 /* Free a codebook.  NULL is ignored. */
 void lloydmax_codebook_destroy(orbit_codebook c);
@@ -145,7 +169,8 @@ void lloydmax_codebook_destroy(orbit_codebook c);
  *   stream  hipStream_t
  *
  * Pointers: W and w_codes 16-byte aligned, w_norm 2-byte aligned.
- * Errors: ORBIT_EINVAL (null pointer, K mismatch, ldw, alignment); ORBIT_EUNSUPPORTED
+ * Errors: ORBIT_EINVAL (null pointer, K mismatch, ldw, alignment, a plan or codebook without
+ * tables on the current device); ORBIT_EUNSUPPORTED
  * (h outside 128..4096, K > 16384, bits not in {2, 3, 4, 6}, more than 2^31 - 1 rows, a row
  * stride ldw - K of 2^23 elements or more);
  * ORBIT_EHIP.  N = 0 returns at once.  Packing as above: at b = 6 every 4 codes fill 3 bytes.

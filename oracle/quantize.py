@@ -62,6 +62,20 @@ def near_tie_mask(U: np.ndarray, thresholds: np.ndarray, band: float) -> np.ndar
     return np.minimum(lo, hi) <= band
 
 
+def nearest_threshold(U: np.ndarray, thresholds: np.ndarray) -> np.ndarray:
+    """Index j of the decision threshold nearest to each coordinate.
+
+    Threshold tau_j is the midpoint of levels j and j+1 (Eq. (3) with the midpoint condition of
+    Lloyd-Max), so at u = tau_j exactly the argmin of Eq. (3) is the pair {j, j+1}: those are the
+    only two codes a nearest-centroid map may return for a coordinate within rounding of tau_j."""
+    U = np.asarray(U, dtype=np.float64)
+    t = np.asarray(thresholds, dtype=np.float64)
+    idx = np.searchsorted(t, U)
+    lo = np.clip(idx - 1, 0, len(t) - 1)
+    hi = np.clip(idx, 0, len(t) - 1)
+    return np.where(np.abs(U - t[lo]) <= np.abs(U - t[hi]), lo, hi)
+
+
 def decode_levels(codes: np.ndarray, levels: np.ndarray) -> np.ndarray:
     return np.asarray(levels)[codes]
 

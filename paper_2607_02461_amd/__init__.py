@@ -32,10 +32,12 @@ SIGNATURES = {
     "rpbh_plan": (ctypes.c_int, [_i64, _i32, _u64, ctypes.POINTER(_c_void_p)]),
     "rpbh_plan_from_arrays": (ctypes.c_int, [_i64, _i32, _c_void_p, _c_void_p, ctypes.POINTER(_c_void_p)]),
     "rpbh_plan_get": (ctypes.c_int, [_c_void_p, ctypes.POINTER(_i64), ctypes.POINTER(_i32), _c_void_p, _c_void_p]),
+    "rpbh_plan_upload": (ctypes.c_int, [_c_void_p]),
     "rpbh_plan_destroy": (None, [_c_void_p]),
     "lloydmax_codebook": (ctypes.c_int, [_i32, _i64, ctypes.POINTER(_c_void_p)]),
     "lloydmax_codebook_get": (ctypes.c_int, [_c_void_p, ctypes.POINTER(_i32), ctypes.POINTER(_i64),
                                              _c_void_p, _c_void_p, _c_void_p]),
+    "lloydmax_codebook_upload": (ctypes.c_int, [_c_void_p]),
     "lloydmax_codebook_destroy": (None, [_c_void_p]),
     "quantize_weights_offline": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i64,
                                                 ctypes.c_float, _c_void_p, _c_void_p, _c_void_p]),
@@ -118,6 +120,13 @@ class Plan:
     def h(self):
         return self._get()[1]
 
+    def upload(self, device=None):
+        """Copies the plan's device tables to `device` (default: the current one), which device
+        calls there need; creation did this for the device current at the time."""
+        with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
+            _check("rpbh_plan_upload", lib().rpbh_plan_upload(self._h))
+        return self
+
     def arrays(self):
         """(perm int32 [d], sign int8 [d]) as numpy arrays."""
         d = self.d
@@ -152,6 +161,12 @@ class Codebook:
     @property
     def handle(self):
         return self._h
+
+    def upload(self, device=None):
+        """Copies the encoder table to `device` (default: the current one), as Plan.upload."""
+        with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
+            _check("lloydmax_codebook_upload", lib().lloydmax_codebook_upload(self._h))
+        return self
 
     def __del__(self):
         if getattr(self, "_h", None) and _lib is not None:

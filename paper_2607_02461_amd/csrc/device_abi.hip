@@ -45,48 +45,86 @@ orbit_status current_device(int* dev, DeviceInfo* info) {
     return ORBIT_OK;
 }
 
-// The plan's tables on device `dev`, uploaded on first use: K gather offsets (2*perm[j], the
-// byte offset of the element that moves to position j, with bit 31 set where sign[j] = -1)
-// followed by K/2 sign masks over positions (bit 15 / bit 31 of word i carry sign[2i] /
-// sign[2i+1]), which the identity-permutation path applies to the pairs it loads.
+// The plan's tables on device `dev`: K gather offsets (2*perm[j], the byte offset of the element
+// that moves to position j, with bit 31 set where sign[j] = -1) followed by K/2 sign masks over
+// positions (bit 15 / bit 31 of word i carry sign[2i] / sign[2i+1]), which the identity-permutation
+// path applies to the pairs it loads.  Built and copied once per device, at set-up (handle creation
+// or an explicit upload), never from a device call.
+orbit_status plan_upload_dev(orbit_plan p, int dev) {
+    std::lock_guard<std::mutex> lk(p->mu);
+    if (p->dev_meta[dev]) return ORBIT_OK;
+    const int64_t d = p->d;
+    std::vector<uint32_t> meta;
+    try {
+        meta.assign((size_t)(d + (d + 1) / 2), 0u);
+    } catch (...) {
+        return fail(ORBIT_ENOMEM, "plan upload: out of host memory");
+    }
+    for (int64_t j = 0; j < d; ++j) {
+        meta[j] = (uint32_t)p->perm[j] * 2u | (p->sign[j] < 0 ? 0x80000000u : 0u);
+        if (p->sign[j] < 0) meta[d + j / 2] |= (j & 1) ? 0x80000000u : 0x8000u;
+    }
+    void* dp = nullptr;
+    hipError_t e = hipMalloc(&dp, meta.size() * sizeof(uint32_t));
+    if (e != hipSuccess)
+        return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "plan upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
+    e = hipMemcpy(dp, meta.data(), meta.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(dp);
+        return hip_fail(e, "plan upload: hipMemcpy");
+    }
+    p->dev_meta[dev] = (uint32_t*)dp;
+    return ORBIT_OK;
+}
+
+// The codebook's encoder table on device `dev`, copied once per device at set-up.
+orbit_status codebook_upload_dev(orbit_codebook c, int dev) {
+    std::lock_guard<std::mutex> lk(c->mu);
+    if (c->dev_enc[dev]) return ORBIT_OK;
+    const size_t bytes = c->enc.bias.size() * sizeof(float);
+    void* d = nullptr;
+    hipError_t e = hipMalloc(&d, bytes);
+    if (e != hipSuccess)
+        return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "codebook upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
+    e = hipMemcpy(d, c->enc.bias.data(), bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(d);
+        return hip_fail(e, "codebook upload: hipMemcpy");
+    }
+    c->dev_enc[dev] = (float*)d;
+    return ORBIT_OK;
+}
+
+// The current device, or -1 when no HIP device is visible (handles then stay host-only).
+orbit_status device_for_upload(int* dev) {
+    int n = 0;
+    if (hipGetDeviceCount(&n) != hipSuccess || n <= 0) {
+        (void)hipGetLastError();  // leave no sticky error behind on a machine without a GPU
+        *dev = -1;
+        return ORBIT_OK;
+    }
+    hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (*dev < 0 || *dev >= kMaxDevices) return fail(ORBIT_EUNSUPPORTED, "device ordinal %d out of range", *dev);
+    return ORBIT_OK;
+}
+
+// Tables of a handle on the device of a call: present since set-up, or the call is refused (a
+// device call only enqueues work; it never allocates or copies synchronously).
 orbit_status plan_meta(orbit_plan p, int dev, const uint32_t** out) {
     std::lock_guard<std::mutex> lk(p->mu);
-    if (!p->dev_meta[dev]) {
-        const int64_t d = p->d;
-        std::vector<uint32_t> meta((size_t)(d + (d + 1) / 2), 0u);
-        for (int64_t j = 0; j < d; ++j) {
-            meta[j] = (uint32_t)p->perm[j] * 2u | (p->sign[j] < 0 ? 0x80000000u : 0u);
-            if (p->sign[j] < 0) meta[d + j / 2] |= (j & 1) ? 0x80000000u : 0x8000u;
-        }
-        void* dp = nullptr;
-        hipError_t e = hipMalloc(&dp, meta.size() * sizeof(uint32_t));
-        if (e != hipSuccess) return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "plan upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
-        e = hipMemcpy(dp, meta.data(), meta.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
-        if (e != hipSuccess) {
-            (void)hipFree(dp);
-            return hip_fail(e, "plan upload: hipMemcpy");
-        }
-        p->dev_meta[dev] = (uint32_t*)dp;
-    }
+    if (!p->dev_meta[dev])
+        return fail(ORBIT_EINVAL, "the plan has no tables on device %d: create it with that device current, or call "
+                                  "rpbh_plan_upload there first", dev);
     *out = p->dev_meta[dev];
     return ORBIT_OK;
 }
 
-// The codebook's encoder table on device `dev`, uploaded on first use.
 orbit_status codebook_enc(orbit_codebook c, int dev, const float** out) {
     std::lock_guard<std::mutex> lk(c->mu);
-    if (!c->dev_enc[dev]) {
-        const size_t bytes = c->enc.bias.size() * sizeof(float);
-        void* d = nullptr;
-        hipError_t e = hipMalloc(&d, bytes);
-        if (e != hipSuccess) return e == hipErrorOutOfMemory ? fail(ORBIT_ENOMEM, "codebook upload: hipMalloc failed") : hip_fail(e, "hipMalloc");
-        e = hipMemcpy(d, c->enc.bias.data(), bytes, hipMemcpyHostToDevice);
-        if (e != hipSuccess) {
-            (void)hipFree(d);
-            return hip_fail(e, "codebook upload: hipMemcpy");
-        }
-        c->dev_enc[dev] = (float*)d;
-    }
+    if (!c->dev_enc[dev])
+        return fail(ORBIT_EINVAL, "the codebook has no encoder table on device %d: create it with that device "
+                                  "current, or call lloydmax_codebook_upload there first", dev);
     *out = c->dev_enc[dev];
     return ORBIT_OK;
 }
@@ -185,7 +223,34 @@ void free_per_device(T* (&ptrs)[kMaxDevices]) {
 
 }  // namespace
 
+orbit_status orbit::upload_on_create(orbit_plan p, orbit_codebook c) {
+    int dev;
+    orbit_status st = device_for_upload(&dev);
+    if (st != ORBIT_OK || dev < 0) return st;
+    return p ? plan_upload_dev(p, dev) : codebook_upload_dev(c, dev);
+}
+
 extern "C" {
+
+orbit_status rpbh_plan_upload(orbit_plan p) {
+    clear_error();
+    if (!p) return fail(ORBIT_EINVAL, "rpbh_plan_upload: plan is NULL");
+    int dev;
+    DeviceInfo info;
+    orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    return plan_upload_dev(p, dev);
+}
+
+orbit_status lloydmax_codebook_upload(orbit_codebook c) {
+    clear_error();
+    if (!c) return fail(ORBIT_EINVAL, "lloydmax_codebook_upload: codebook is NULL");
+    int dev;
+    DeviceInfo info;
+    orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    return codebook_upload_dev(c, dev);
+}
 
 void rpbh_plan_destroy(orbit_plan p) {
     if (!p) return;

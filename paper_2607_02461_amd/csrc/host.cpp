@@ -333,6 +333,11 @@ orbit_status rpbh_plan_from_arrays(int64_t d, int32_t h, const int32_t* perm, co
     p->h = h;
     p->identity = true;
     for (int64_t j = 0; j < d && p->identity; ++j) p->identity = p->perm[j] == j;
+    const orbit_status st = upload_on_create(p, nullptr);
+    if (st != ORBIT_OK) {
+        rpbh_plan_destroy(p);
+        return st;
+    }
     *out = p;
     return ORBIT_OK;
 }
@@ -398,6 +403,11 @@ orbit_status lloydmax_codebook(int32_t bits, int64_t d, orbit_codebook* out) {
         uint16_t bitsv;
         std::memcpy(&bitsv, &hv, 2);
         c->lut_f16[j] = bitsv;
+    }
+    const orbit_status st = upload_on_create(nullptr, c);
+    if (st != ORBIT_OK) {
+        lloydmax_codebook_destroy(c);
+        return st;
     }
     *out = c;
     return ORBIT_OK;

@@ -26,7 +26,8 @@ struct orbit_plan_s {
     std::vector<int32_t> perm;  // y_j = x[perm[j]]
     std::vector<int8_t> sign;   // multiplies post-permutation coordinate j
     bool identity = false;      // perm[j] == j for every j (Block-RHT, full-dimension rotations)
-    // Per-device tables for the quantizer (gather offsets and sign masks), see plan_meta().
+    // Per-device tables for the quantizer (gather offsets and sign masks), set up at creation or by
+    // rpbh_plan_upload, see plan_upload_dev().
     std::mutex mu;
     uint32_t* dev_meta[orbit::kMaxDevices] = {};
 };
@@ -60,4 +61,7 @@ struct orbit_codebook_s {
 
 namespace orbit {
 void build_enc_table(orbit_codebook_s* c);
+// Set-up of a new handle (exactly one of p, c non-null): copies its device tables to the current
+// device when a HIP device is visible; a machine without one keeps host-only handles.
+orbit_status upload_on_create(orbit_plan_s* p, orbit_codebook_s* c);
 }

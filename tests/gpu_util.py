@@ -14,6 +14,22 @@ import paper_2607_02461_amd as oq
 
 TIE_BAND = 1e-5      # |u - tau| at or below this is a near-tie: counted, not a failure
 GEMM_REL_F = 2e-3    # relative Frobenius bar for the GEMM against fp64 with identical codes/levels
+# Per-element bar of the contraction: |Y[n,i] - ref[n,i]| <= ELEM_TOL * s_n r'_i ||a_n|| ||b_i||, with
+# a_n = L_a[x_code[n]] and b_i = L_w[w_code[i]] (fp16 levels).  The fp16 products are exact in fp32;
+# what remains is the fp32 sum of K of them (plus split partials and a few epilogue roundings).  The
+# probabilistic bound on a sum of n terms (Higham and Mary, SIAM J. Sci. Comput. 2019),
+# lambda sqrt(n) u sum|a_k b_k| with u = 2^-24 and lambda = 10, is below 8e-5 ||a|| ||b|| (Cauchy-Schwarz)
+# for n up to 16384 + 64, so 1e-4 holds with margin for every K these tests use up to 16384; the
+# K = 65536 cases take the same formula at their n (1.5e-4).  A wrong tile, a dropped K-step or a
+# misplaced row fails it at once: such errors are of the order of the outputs themselves,
+# ~||a|| ||b|| / sqrt(K).
+ELEM_TOL = 1e-4
+
+
+def elem_tol(K: int) -> float:
+    """The per-element bar for a contraction of length K (see ELEM_TOL)."""
+    n = K + 64
+    return max(ELEM_TOL, 10.0 * np.sqrt(n) * 2.0 ** -24)
 
 
 def log_stats(name, **stats):
@@ -58,9 +74,7 @@ def compare_quantizer(name, X: torch.Tensor, bits: int, seed: int = 0, weights: 
         oc, on, U = oracle.quantize_act(Xs, oplan, ocb, eps)
     gcodes = codes.cpu().numpy()[sel]
     gc = oracle.unpack_codes(gcodes, bits, K)
-    near = oracle.near_tie_mask(U, ocb.thresholds, TIE_BAND)
-    mism = gc != oc
-    bad = int(np.sum(mism & ~near))
+    cstats = code_stats(gc, oc, U, ocb.thresholds)
     if weights:
         gn = norms.float().cpu().numpy().astype(np.float64)[sel]
         ulp = np.ldexp(1.0, np.frexp(np.maximum(on, 1e-30))[1] - 8)
@@ -70,13 +84,35 @@ def compare_quantizer(name, X: torch.Tensor, bits: int, seed: int = 0, weights: 
         gn = norms.cpu().numpy().astype(np.float64)[sel]
         norm_err = float(np.max(np.abs(gn - on) / np.maximum(on, 1e-30))) if len(on) else 0.0
         norm_ok = norm_err <= 1e-5 or bool(np.all(np.abs(gn - on) <= 1e-30))
-    log_stats(name, M=M, K=K, h=oplan.h, bits=bits, weights=weights, rows_checked=len(sel), elements=int(gc.size),
-              near_ties=int(near.sum()), near_tie_frac=float(near.mean()) if near.size else 0.0,
-              near_tie_mismatches=int(np.sum(mism & near)), mismatches_off_tie=bad,
+    log_stats(name, M=M, K=K, h=oplan.h, bits=bits, weights=weights, rows_checked=len(sel), **cstats,
               norm_err=norm_err)
-    assert bad == 0, f"{name}: {bad} code mismatches farther than {TIE_BAND} from a threshold"
+    assert_codes(name, cstats)
     assert norm_ok, f"{name}: norm error {norm_err}"
     return codes, norms
+
+
+def code_stats(gc, oc, U, thresholds, band=TIE_BAND) -> dict:
+    """Counts of a comparison of the HIP path's codes `gc` with the oracle's `oc` (both unpacked).
+
+    Off near-ties the codes must be equal.  Within `band` of a threshold tau_j the nearest-centroid
+    map of Eq. (3) ties between codes j and j+1 at tau_j itself, so either is correct there and
+    nothing else is: a near-tie code outside that pair is invalid."""
+    near = oracle.near_tie_mask(U, thresholds, band)
+    mism = gc != oc
+    j = oracle.nearest_threshold(U, thresholds)
+    pair = (gc == j) | (gc == j + 1)
+    return dict(elements=int(gc.size), near_ties=int(near.sum()),
+                near_tie_frac=float(near.mean()) if near.size else 0.0,
+                near_tie_mismatches=int(np.sum(mism & near)),
+                near_tie_invalid=int(np.sum(mism & near & ~pair)),
+                mismatches_off_tie=int(np.sum(mism & ~near)))
+
+
+def assert_codes(name, stats):
+    assert stats["mismatches_off_tie"] == 0, \
+        f"{name}: {stats['mismatches_off_tie']} code mismatches farther than {TIE_BAND} from a threshold"
+    assert stats["near_tie_invalid"] == 0, \
+        f"{name}: {stats['near_tie_invalid']} near-tie codes neither the oracle's nor its neighbour across the threshold"
 
 
 def qlinear_oracle_fp16(xc, xs, cba_bits, wc, wr, cbw_bits, K):
@@ -88,6 +124,31 @@ def qlinear_oracle_fp16(xc, xs, cba_bits, wc, wr, cbw_bits, K):
 
 def rel_frobenius(a, b):
     return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def gemm_scale(xc, s, la, wc, r, lw) -> np.ndarray:
+    """s_n r'_i ||L_a[x_code[n]]|| ||L_w[w_code[i]]||: the Cauchy-Schwarz bound on |Y[n,i]|, the
+    unit of the per-element bar."""
+    la, lw = np.asarray(la, dtype=np.float64), np.asarray(lw, dtype=np.float64)
+    na = np.linalg.norm(la[np.asarray(xc)], axis=1)
+    nb = np.linalg.norm(lw[np.asarray(wc)], axis=1)
+    return (np.asarray(s, dtype=np.float64) * na)[:, None] * (np.asarray(r, dtype=np.float64) * nb)[None, :]
+
+
+def check_gemm(name, Y, ref, scale, K, slack=0.0, **extra) -> dict:
+    """fp32 layer output `Y` against the fp64 oracle `ref` on identical codes, levels and norms:
+    relative Frobenius error <= GEMM_REL_F, and every element within elem_tol(K) * scale (+ slack,
+    an epilogue's own allowance).  Returns and logs the figures."""
+    Y = np.asarray(Y, dtype=np.float64)
+    err = rel_frobenius(Y, ref)
+    tol = elem_tol(K)
+    excess = np.abs(Y - ref) - (tol * scale + slack)
+    worst = float(np.max(np.abs(Y - ref) / np.maximum(tol * scale + slack, 1e-300))) if Y.size else 0.0
+    stats = dict(rel_f=err, worst_elem_over_bar=worst, elems_beyond_bar=int(np.sum(excess > 0)), **extra)
+    log_stats(name, **stats)
+    assert err <= GEMM_REL_F, f"{name}: relative Frobenius error {err}"
+    assert stats["elems_beyond_bar"] == 0, f"{name}: {stats['elems_beyond_bar']} outputs beyond the per-element bar"
+    return stats
 
 
 def near_tie_flip_bound(cx, s, Ux, la, tha, cw, r, Uw, lw, thw, band=TIE_BAND):

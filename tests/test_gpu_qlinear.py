@@ -10,7 +10,8 @@ import torch
 import oracle
 import paper_2607_02461_amd as oq
 from paper_2607_02461_amd import workloads
-from tests.gpu_util import GEMM_REL_F, log_stats, near_tie_flip_bound, qlinear_oracle_fp16, rel_frobenius, to_f64
+from tests.gpu_util import (GEMM_REL_F, check_gemm, gemm_scale, log_stats, near_tie_flip_bound, qlinear_oracle_fp16,
+                            rel_frobenius, to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -23,6 +24,13 @@ def _inputs(M, N, K, ba, bw, seed):
     xs = workloads.random_norms(M, seed, 0)
     wr = workloads.random_norms(N, seed, 1).to(torch.bfloat16)
     return xc, xs, wc, wr
+
+
+def _scale(xc, xs, ba, wc, wr, bw, K):
+    """Per-element unit s_n r'_i ||a_n|| ||b_i|| on the oracle's fp16 levels."""
+    la = oracle.fp16_round(oracle.lloydmax_codebook(ba, K).levels)
+    lw = oracle.fp16_round(oracle.lloydmax_codebook(bw, K).levels)
+    return gemm_scale(xc, xs, la, wc, wr, lw)
 
 
 def _gpu(xc, xs, wc, wr, ba, bw, K):
@@ -42,10 +50,8 @@ def _gpu(xc, xs, wc, wr, ba, bw, K):
 def test_random_codes(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
-    ref = qlinear_oracle_fp16(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
-    err = rel_frobenius(Y, ref)
-    log_stats(f"gemm random M={M} N={N} K={K} W{bw}A{ba}", rel_f=err)
-    assert err <= GEMM_REL_F
+    args = (xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
+    check_gemm(f"gemm random M={M} N={N} K={K} W{bw}A{ba}", Y, qlinear_oracle_fp16(*args), _scale(*args), K)
 
 
 # shapes with at least one 256x256 tile per compute unit (256) run the large-tile kernel; these
@@ -60,11 +66,10 @@ def test_random_codes(M, N, K, ba, bw):
 def test_random_codes_large_tiles(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
-    ref = qlinear_oracle_fp16(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
-    err = rel_frobenius(Y, ref)
+    args = (xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
+    ref = qlinear_oracle_fp16(*args)
     worst_row = float(np.max(np.linalg.norm(Y - ref, axis=1) / np.maximum(np.linalg.norm(ref, axis=1), 1e-300)))
-    log_stats(f"gemm large-tile M={M} N={N} K={K} W{bw}A{ba}", rel_f=err, worst_row_rel=worst_row)
-    assert err <= GEMM_REL_F
+    check_gemm(f"gemm large-tile M={M} N={N} K={K} W{bw}A{ba}", Y, ref, _scale(*args), K, worst_row_rel=worst_row)
     assert worst_row <= GEMM_REL_F
 
 
@@ -93,6 +98,13 @@ def test_fused_epilogue(M, N, K, bias, gelu, bf16, pad):
     ref = oracle.layer_epilogue(base, bias=b.double().numpy() if bias else None, gelu=gelu)
     err = rel_frobenius(Yn, ref)
     stats = {"rel_f": err}
+    if not bf16:
+        # fp32 outputs: the contraction's per-element bar, carried through GELU (slope below 1.13),
+        # plus the epilogue's own roundings (the rescale, the bias add, the erfc form's 1.2e-7)
+        scale = _scale(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
+        pre = np.abs(base) + (np.abs(b.double().numpy())[None, :] if bias else 0.0)
+        check_gemm(f"fused epilogue fp32 M={M} N={N} K={K} bias={bias} gelu={gelu} pad={pad}", Yn, ref,
+                   1.13 * scale if gelu else scale, K, slack=1e-6 * pre)
     if bf16:
         # every bf16 output is the rounding of a value within the fp32 accumulation error of the
         # fp64 result: at most one bf16 ulp from it, plus an absolute slack of 1e-5 of the
@@ -147,9 +159,10 @@ def test_c4_up_shape_sampled_rows():
     ridx = torch.as_tensor(rows, device=DEV)
     ref = qlinear_oracle_fp16(xc[ridx].cpu().numpy(), xs[ridx].double().cpu().numpy(), 4,
                               wc.cpu().numpy(), wr.double().cpu().numpy(), 4, K)
-    err = rel_frobenius(Y[ridx].double().cpu().numpy(), ref)
-    log_stats("gemm c4 up sampled", rel_f=err, rows=len(rows))
-    assert err <= GEMM_REL_F
+    la = oracle.fp16_round(oracle.lloydmax_codebook(4, K).levels)
+    scale = gemm_scale(xc[ridx].cpu().numpy(), xs[ridx].double().cpu().numpy(), la, wc.cpu().numpy(),
+                       wr.double().cpu().numpy(), la)
+    check_gemm("gemm c4 up sampled", Y[ridx].double().cpu().numpy(), ref, scale, K, rows=len(rows))
 
 
 @pytest.mark.parametrize("bw,ba", [(4, 4), (3, 4), (2, 4), (3, 3), (4, 6)])
@@ -220,10 +233,8 @@ def test_long_contraction(ba, bw):
     M, N, K = 300, 260, 65536
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=K + ba)
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
-    ref = qlinear_oracle_fp16(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
-    err = rel_frobenius(Y, ref)
-    log_stats(f"gemm long K={K} W{bw}A{ba}", rel_f=err)
-    assert err <= GEMM_REL_F
+    args = (xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
+    check_gemm(f"gemm long K={K} W{bw}A{ba}", Y, qlinear_oracle_fp16(*args), _scale(*args), K)
 
 
 def test_long_contraction_large_tiles_sampled_rows():
@@ -233,10 +244,8 @@ def test_long_contraction_large_tiles_sampled_rows():
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
     rows = np.sort(np.random.default_rng(9).choice(M, 64, replace=False))
     rows[-1] = M - 1
-    ref = qlinear_oracle_fp16(xc.numpy()[rows], xs.double().numpy()[rows], ba, wc.numpy(), wr.double().numpy(), bw, K)
-    err = rel_frobenius(Y[rows], ref)
-    log_stats(f"gemm long large-tile K={K}", rel_f=err, rows=len(rows))
-    assert err <= GEMM_REL_F
+    args = (xc.numpy()[rows], xs.double().numpy()[rows], ba, wc.numpy(), wr.double().numpy(), bw, K)
+    check_gemm(f"gemm long large-tile K={K}", Y[rows], qlinear_oracle_fp16(*args), _scale(*args), K, rows=len(rows))
 
 
 def test_empty_operands_are_noops():

@@ -11,7 +11,7 @@ import torch
 import oracle
 import paper_2607_02461_amd as oq
 from paper_2607_02461_amd import workloads
-from tests.gpu_util import GEMM_REL_F, log_stats, qlinear_oracle_fp16, rel_frobenius
+from tests.gpu_util import GEMM_REL_F, check_gemm, gemm_scale, log_stats, qlinear_oracle_fp16, rel_frobenius
 
 pytestmark = pytest.mark.gpu
 
@@ -27,6 +27,13 @@ def _operands(M, N, K, ba, bw, seed):
     dev = (torch.from_numpy(oracle.pack_codes(xc.numpy(), ba)).to(DEV), xs.to(DEV),
            torch.from_numpy(oracle.pack_codes(wc.numpy(), bw)).to(DEV), wr.to(DEV))
     return (xc, xs, wc, wr), (cba, cbw), dev
+
+
+def _scale(xc, xs, ba, wc, wr, bw, K):
+    """Per-element unit s_n r'_i ||a_n|| ||b_i|| on the oracle's fp16 levels."""
+    la = oracle.fp16_round(oracle.lloydmax_codebook(ba, K).levels)
+    lw = oracle.fp16_round(oracle.lloydmax_codebook(bw, K).levels)
+    return gemm_scale(xc, xs, la, wc, wr, lw)
 
 
 def _workspace(M, N, K, fill=float("nan")):
@@ -57,10 +64,11 @@ def test_split_matches_oracle_and_unsplit(M, N, K, ba, bw):
     torch.cuda.synchronize()
     Y, Y0 = Y.cpu().numpy().astype(np.float64), Y0.cpu().numpy().astype(np.float64)
     xc, xsh, wc, wrh = host
-    ref = qlinear_oracle_fp16(xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
-    err, err0, d = rel_frobenius(Y, ref), rel_frobenius(Y0, ref), rel_frobenius(Y, Y0)
-    log_stats(f"split M={M} N={N} K={K} W{bw}A{ba} splits={S}", rel_f=err, rel_f_unsplit=err0, vs_unsplit=d)
-    assert err <= GEMM_REL_F
+    args = (xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
+    ref = qlinear_oracle_fp16(*args)
+    err0, d = rel_frobenius(Y0, ref), rel_frobenius(Y, Y0)
+    check_gemm(f"split M={M} N={N} K={K} W{bw}A{ba} splits={S}", Y, ref, _scale(*args), K, rel_f_unsplit=err0,
+               vs_unsplit=d)
     assert d <= 1e-5
 
 
@@ -81,11 +89,10 @@ def test_split_tail_of_large_grid(M, N, K):
     rows = np.unique(np.concatenate([np.random.default_rng(K).choice(M, 48, replace=False),
                                      np.arange(M - 16, M)]))
     xc, xsh, wc, wrh = host
-    ref = qlinear_oracle_fp16(xc.numpy()[rows], xsh.double().numpy()[rows], ba, wc.numpy(), wrh.double().numpy(),
-                              bw, K)
-    err, d = rel_frobenius(Y[rows], ref), rel_frobenius(Y, Y0)
-    log_stats(f"split tail M={M} N={N} K={K} workspace={n}", rel_f=err, vs_unsplit=d)
-    assert err <= GEMM_REL_F
+    args = (xc.numpy()[rows], xsh.double().numpy()[rows], ba, wc.numpy(), wrh.double().numpy(), bw, K)
+    d = rel_frobenius(Y, Y0)
+    check_gemm(f"split tail M={M} N={N} K={K} workspace={n}", Y[rows], qlinear_oracle_fp16(*args), _scale(*args), K,
+               vs_unsplit=d)
     assert d <= 1e-5
 
 
@@ -99,10 +106,9 @@ def test_split_remaining_bit_pairs(M, N, K, ba, bw):
     Y = oq.orbit_qlinear_ws(cba, xp, xs, cbw, wp, wr, ws)
     torch.cuda.synchronize()
     xc, xsh, wc, wrh = host
-    ref = qlinear_oracle_fp16(xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
-    err = rel_frobenius(Y.cpu().numpy().astype(np.float64), ref)
-    log_stats(f"split bits M={M} N={N} K={K} W{bw}A{ba}", rel_f=err)
-    assert err <= GEMM_REL_F
+    args = (xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
+    check_gemm(f"split bits M={M} N={N} K={K} W{bw}A{ba}", Y.cpu().numpy().astype(np.float64),
+               qlinear_oracle_fp16(*args), _scale(*args), K)
 
 
 @pytest.mark.parametrize("bias,gelu,bf16", [(True, False, False), (False, True, False), (False, False, True),
@@ -134,6 +140,13 @@ def test_split_fused_epilogue(bias, gelu, bf16, pad):
         assert not (np.abs(Yn - ref) > ulp + 1e-5 * np.max(np.abs(ref))).any()
         assert np.mean(Yn == rb) > 0.999
         ref = rb
+    else:
+        # fp32 outputs: the per-element bar through GELU's slope (below 1.13) plus the epilogue's
+        # own roundings
+        scale = _scale(xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
+        pre = np.abs(base) + (np.abs(bd)[None, :] if bias else 0.0)
+        check_gemm(f"split epilogue fp32 bias={bias} gelu={gelu} pad={pad}", Yn, ref, 1.13 * scale if gelu else scale,
+                   K, slack=1e-6 * pre)
     err = rel_frobenius(Yn, ref)
     log_stats(f"split epilogue bias={bias} gelu={gelu} bf16={bf16} pad={pad}", rel_f=err)
     assert err <= GEMM_REL_F
@@ -163,8 +176,9 @@ def test_workspace_reused_across_shapes():
         outs.append((host, K, oq.orbit_qlinear_ws(cba, xp, xs, cbw, wp, wr, ws)))
     torch.cuda.synchronize()
     for (xc, xsh, wc, wrh), K, Y in outs:
-        ref = qlinear_oracle_fp16(xc.numpy(), xsh.double().numpy(), 4, wc.numpy(), wrh.double().numpy(), 3, K)
-        assert rel_frobenius(Y.cpu().numpy().astype(np.float64), ref) <= GEMM_REL_F
+        args = (xc.numpy(), xsh.double().numpy(), 4, wc.numpy(), wrh.double().numpy(), 3, K)
+        check_gemm(f"split workspace reuse K={K}", Y.cpu().numpy().astype(np.float64), qlinear_oracle_fp16(*args),
+                   _scale(*args), K)
 
 
 def test_small_or_missing_workspace_runs_unsplit():

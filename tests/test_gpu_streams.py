@@ -1,8 +1,9 @@
 """Streams and graph capture through the C ABI: device calls only enqueue on the caller's stream,
-handles may be shared by calls on several streams at once, and once a plan and codebook have been
-used on the device (their tables uploaded), the quantizer and the layer (also split over K with a
-workspace) can be captured in a HIP graph and replayed.  Every kernel is deterministic, so each
-result is compared bit for bit with the same call made eagerly on the default stream."""
+handles may be shared by calls on several streams at once, and the quantizer and the layer (also
+split over K with a workspace) can be captured in a HIP graph and replayed, from the very first
+call that uses a new plan and codebook (their device tables are set up when the handles are
+created).  Every kernel is deterministic, so each result is compared bit for bit with the same
+call made eagerly on the default stream."""
 
 import numpy as np
 import pytest
@@ -68,7 +69,7 @@ def test_graph_capture_and_replay():
         oq.rpbh_quantize_act(plan, cb, X, 1e-10, xc, xn)
         oq.orbit_qlinear_ex(cb, xc, xn, cb, wc, wn, bias=bias, gelu=True, out_dtype=torch.bfloat16, out=Y)
 
-    step()                       # eager first call: uploads the plan and codebook tables
+    step()                       # eager first call
     torch.cuda.synchronize()
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
@@ -160,3 +161,47 @@ def test_split_layers_on_two_streams_with_their_own_workspaces():
     torch.cuda.synchronize()
     for i in range(2):
         assert torch.equal(out[i], ref[i]), f"stream {i}: results differ from the default-stream call"
+
+
+def test_first_call_of_new_handles_is_captured():
+    # handles created just before the capture, with no eager call of theirs: the weight pass, the
+    # quantizer and the layer record only kernel launches, and every replay (with eager work and
+    # overwritten outputs between replays) equals the same calls made eagerly afterwards
+    K, M, N = 3072, 1000, 2048
+    plan = oq.rpbh_plan(K, 128, 11)
+    cb_a, cb_w = oq.lloydmax_codebook(4, K), oq.lloydmax_codebook(3, K)
+    X, W = _bf16(M, K, 50), _bf16(N, K, 51, scale=0.02)
+    wc = torch.empty((N, K * 3 // 8), dtype=torch.uint8, device=DEV)
+    wn = torch.empty((N,), dtype=torch.bfloat16, device=DEV)
+    xc = torch.empty((M, K // 2), dtype=torch.uint8, device=DEV)
+    xn = torch.empty((M,), dtype=torch.float32, device=DEV)
+    Y = torch.empty((M, N), dtype=torch.float32, device=DEV)
+
+    def step(outs):
+        wc_, wn_, xc_, xn_, Y_ = outs
+        oq.quantize_weights_offline(plan, cb_w, W, 1e-10, wc_, wn_)
+        oq.rpbh_quantize_act(plan, cb_a, X, 1e-10, xc_, xn_)
+        oq.orbit_qlinear(cb_a, xc_, xn_, cb_w, wc_, wn_, out=Y_)
+
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step((wc, wn, xc, xn, Y))
+    torch.cuda.synchronize()
+    replays = []
+    for r in range(3):
+        for t in (wc, xc):
+            t.fill_(0xA5)
+        for t in (wn, xn, Y):
+            t.fill_(float("nan"))
+        _ = _bf16(512, 512, 60 + r).float().sum()     # unrelated eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        replays.append([t.clone() for t in (wc, wn, xc, xn, Y)])
+    eager = [torch.empty_like(t) for t in (wc, wn, xc, xn, Y)]
+    step(eager)
+    torch.cuda.synchronize()
+    for r, got in enumerate(replays):
+        for a, b, name in zip(got, eager, ("weight codes", "weight norms", "codes", "norms", "Y")):
+            assert torch.equal(a, b), f"replay {r}: {name} differ from the eager calls"

@@ -173,6 +173,25 @@ def test_near_tie_mask_matches_bruteforce_distance():
     assert np.array_equal(oracle.near_tie_mask(u, cb.thresholds, 1e-5), brute)
 
 
+@pytest.mark.parametrize("bits", [2, 3, 4, 6])
+def test_nearest_threshold_pairs_are_the_two_nearest_levels(bits):
+    # the nearest threshold's index j names the two codes that are nearest at a near-tie: by brute
+    # force over all levels, the two levels closest to u are j and j+1 for every u within 1e-5 of a
+    # threshold, and j is the argmin of |u - tau| everywhere
+    cb = _cb(bits, 3072)
+    rng = np.random.default_rng(bits)
+    near = np.concatenate([cb.thresholds + d for d in (0.0, 3e-6, -7e-6, 1e-5, -1e-5)])
+    u = np.concatenate([rng.normal(size=3000) / math.sqrt(3072), near])
+    j = oracle.nearest_threshold(u, cb.thresholds)
+    assert np.array_equal(j, np.argmin(np.abs(u[:, None] - cb.thresholds[None, :]), axis=1))
+    two = np.sort(np.argsort(np.abs(near[:, None] - cb.levels[None, :]), axis=1, kind="stable")[:, :2], axis=1)
+    jn = oracle.nearest_threshold(near, cb.thresholds)
+    assert np.array_equal(two[:, 0], jn) and np.array_equal(two[:, 1], jn + 1)
+    # the oracle's own code is one of the pair
+    c = oracle.encode(near, cb.thresholds)
+    assert np.all((c == jn) | (c == jn + 1))
+
+
 def test_layer_epilogue_closed_forms():
     # GELU(x) = x * Phi(x): Phi(1) = 0.841344746068543, Phi(-1) = 1 - Phi(1), GELU(0) = 0, and
     # GELU(x) - GELU(-x) = x for every x
