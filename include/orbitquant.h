@@ -265,6 +265,19 @@ orbit_status orbit_qlinear_ex(orbit_codebook cb_a, const uint8_t* x_codes, const
 orbit_status orbit_qlinear_workspace_size(int64_t M, int64_t N, int64_t K, size_t* bytes);
 
 /*
+ * orbit_qlinear_schedule -- how the layer kernels run an M x N x K layer on the current device:
+ * output rows [0, rows_large) on the 256 x 256-tile kernel, rows [rows_large, M) on the
+ * 128 x 128-tile kernel, the latter split over K into `splits` contiguous ranges (1 = unsplit)
+ * when orbit_qlinear_ws has a workspace of orbit_qlinear_workspace_size(M, N, K) bytes.  For
+ * profiling and for callers that time or place the two parts themselves; the layer calls make the
+ * same choice internally.
+ *   rows_large, splits  host, out
+ * Errors: ORBIT_EINVAL (null outputs, negative M or N, K not a positive multiple of 64 up to
+ * 2^30); ORBIT_EHIP (no device).  M = 0 or N = 0 gives 0 and 1.
+ */
+orbit_status orbit_qlinear_schedule(int64_t M, int64_t N, int64_t K, int64_t* rows_large, int32_t* splits);
+
+/*
  * orbit_qlinear_ws -- orbit_qlinear_ex with a caller-owned device workspace.  With
  * workspace_bytes at least orbit_qlinear_workspace_size(M, N, K) on the same device (and the
  * workspace 16-byte aligned) the rows of a small grid run split over K: the splits' fp32 sums

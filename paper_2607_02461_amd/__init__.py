@@ -49,6 +49,7 @@ SIGNATURES = {
                                         _c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _c_void_p, _i64,
                                         _c_void_p]),
     "orbit_qlinear_workspace_size": (ctypes.c_int, [_i64, _i64, _i64, ctypes.POINTER(ctypes.c_size_t)]),
+    "orbit_qlinear_schedule": (ctypes.c_int, [_i64, _i64, _i64, ctypes.POINTER(_i64), ctypes.POINTER(_i32)]),
     "orbit_qlinear_ws": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
                                         _c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _c_void_p, _i64,
                                         _c_void_p, ctypes.c_size_t, _c_void_p]),
@@ -320,6 +321,16 @@ def orbit_qlinear_workspace_size(M: int, N: int, K: int, device=None) -> int:
     with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
         _check("orbit_qlinear_workspace_size", lib().orbit_qlinear_workspace_size(M, N, K, ctypes.byref(n)))
     return n.value
+
+
+def orbit_qlinear_schedule(M: int, N: int, K: int, device=None):
+    """(rows_large, splits): rows [0, rows_large) of an M x N x K layer run on the 256 x 256 kernel,
+    the rest on the 128 x 128 kernel split `splits` ways over K when given a workspace."""
+    rows, splits = _i64(0), _i32(1)
+    with torch.cuda.device(device if device is not None else torch.cuda.current_device()):
+        _check("orbit_qlinear_schedule", lib().orbit_qlinear_schedule(M, N, K, ctypes.byref(rows),
+                                                                       ctypes.byref(splits)))
+    return rows.value, splits.value
 
 
 def orbit_qlinear_ws(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor, cb_w: Codebook,

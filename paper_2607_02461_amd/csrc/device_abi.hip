@@ -434,4 +434,24 @@ orbit_status orbit_qlinear_workspace_size(int64_t M, int64_t N, int64_t K, size_
     return ORBIT_OK;
 }
 
+orbit_status orbit_qlinear_schedule(int64_t M, int64_t N, int64_t K, int64_t* rows_large, int32_t* splits) {
+    clear_error();
+    if (!rows_large || !splits) return fail(ORBIT_EINVAL, "orbit_qlinear_schedule: null output pointer");
+    *rows_large = 0;
+    *splits = 1;
+    if (M < 0 || N < 0) return fail(ORBIT_EINVAL, "orbit_qlinear_schedule: negative M or N");
+    if (K <= 0 || K % 64 != 0 || K > (int64_t)1 << 30)
+        return fail(ORBIT_EINVAL, "orbit_qlinear_schedule: K=%lld must be a positive multiple of 64", (long long)K);
+    if (M == 0 || N == 0) return ORBIT_OK;
+    int dev;
+    DeviceInfo info;
+    orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    *rows_large = lut_gemm_big_rows(M, N, info.cus);
+    const int64_t m_small = M - *rows_large;
+    int steps = 0;
+    *splits = m_small > 0 ? lut_gemm_small_splits(m_small, N, K, info.cus, &steps) : 1;
+    return ORBIT_OK;
+}
+
 }  // extern "C"

@@ -206,3 +206,21 @@ def test_workspace_size_rules():
     assert oq.orbit_qlinear_workspace_size(0, 3072, 3072) == 0
     n = oq.orbit_qlinear_workspace_size(1, 128, 65536)
     assert _splits(1, 128, 65536, n) >= 2
+
+
+def test_schedule_matches_the_workspace_size():
+    # the schedule query names the rows each kernel runs and the split count; the workspace size
+    # follows from it (splits x rows on the 128 x 128 kernel x N x 4 bytes when it splits)
+    cases = [(256, 3072, 3072), (workloads.C4_M, 5120, 13824), (workloads.C4_M, 13824, 5120), (4133, 8061, 192),
+             (1, 3072, 3072)]
+    for M, N, K in cases:
+        rows, splits = oq.orbit_qlinear_schedule(M, N, K)
+        assert 0 <= rows <= M and splits >= 1
+        want = splits * (M - rows) * N * 4 if splits > 1 else 0
+        assert oq.orbit_qlinear_workspace_size(M, N, K) == want
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        # on 256 compute units: c1 all on the small kernel, five splits; c4's up-projection all on
+        # the large one; its down-projection 32768 rows (ten full rounds) large, 504 split three ways
+        assert oq.orbit_qlinear_schedule(256, 3072, 3072) == (0, 5)
+        assert oq.orbit_qlinear_schedule(workloads.C4_M, 13824, 5120) == (workloads.C4_M, 1)
+        assert oq.orbit_qlinear_schedule(workloads.C4_M, 5120, 13824) == (32768, 3)

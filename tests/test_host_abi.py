@@ -289,3 +289,18 @@ def test_quantizer_rejects_row_gaps_of_2_23_elements():
     st, msg = _status(lib.quantize_weights_offline, p.handle, cb.handle, fake, 4, 256, 256 + (1 << 23), 1e-10, fake,
                       fake, null)
     assert st == oq.ORBIT_EUNSUPPORTED and "stride" in msg
+
+
+def test_qlinear_schedule_validates_and_needs_a_device():
+    lib = oq.lib()
+    rows, splits = ctypes.c_int64(5), ctypes.c_int32(5)
+    st, _ = _status(lib.orbit_qlinear_schedule, 4, 4, 256, None, ctypes.byref(splits))
+    assert st == oq.ORBIT_EINVAL
+    for M, N, K in ((-1, 4, 256), (4, -1, 256), (4, 4, 0), (4, 4, 100)):
+        st, _ = _status(lib.orbit_qlinear_schedule, M, N, K, ctypes.byref(rows), ctypes.byref(splits))
+        assert st == oq.ORBIT_EINVAL and rows.value == 0 and splits.value == 1
+    st, _ = _status(lib.orbit_qlinear_schedule, 0, 3072, 3072, ctypes.byref(rows), ctypes.byref(splits))
+    assert st == oq.ORBIT_OK and rows.value == 0 and splits.value == 1
+    if not torch.cuda.is_available():
+        st, msg = _status(lib.orbit_qlinear_schedule, 256, 3072, 3072, ctypes.byref(rows), ctypes.byref(splits))
+        assert st == oq.ORBIT_EHIP and msg
