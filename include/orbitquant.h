@@ -297,6 +297,27 @@ orbit_status orbit_qlinear_ws(orbit_codebook cb_a, const uint8_t* x_codes, const
                               int64_t ldy, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * orbit_qlinear_noalloc -- orbit_qlinear_ws for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the same layer,
+ * split over K exactly as orbit_qlinear_ws splits it with a large enough workspace (so the same
+ * bits), with the partial sums in a scratch array the library holds in device memory instead of a
+ * caller workspace.  The call allocates nothing and calls no allocating routine.
+ *   Limit: the scratch array is 32 MiB (33554432 bytes) per device, held by every device the
+ *   library runs on until the process ends.  A layer whose split needs more
+ *   (orbit_qlinear_workspace_size(M, N, K) > 32 MiB) returns ORBIT_EUNSUPPORTED; layers that do not
+ *   split need none.
+ *   Sharing: all calls on one device share its scratch array.  Calls that overlap in time on one
+ *   device (on several streams, or from several threads without ordering) race on it and give
+ *   undefined results; serialize them, e.g. on one stream.  The array keeps the last call's
+ *   contents; nothing in it has to start at zero (every partial sum is written before it is read).
+ *   Arguments, other limits and errors as for orbit_qlinear_ex.
+ */
+orbit_status orbit_qlinear_noalloc(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                                   orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
+                                   int64_t K, const uint16_t* bias, int32_t act, int32_t out_dtype, void* Y,
+                                   int64_t ldy, void* stream);
+
+/*
  * adaln_int4_quantize_weights -- the offline pass of the adjacent layer type: the adaptive-layer-
  * norm modulation projections, which the paper keeps at INT4 weight round-to-nearest with group
  * size 64 and BF16 activations, unrotated (Sec. 5 setup; supplementary layer list; Sec. 6.2

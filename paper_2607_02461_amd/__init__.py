@@ -53,6 +53,9 @@ SIGNATURES = {
     "orbit_qlinear_ws": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
                                         _c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _c_void_p, _i64,
                                         _c_void_p, ctypes.c_size_t, _c_void_p]),
+    "orbit_qlinear_noalloc": (ctypes.c_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _c_void_p, _c_void_p,
+                                             _c_void_p, _i64, _i64, _c_void_p, _i32, _i32, _c_void_p, _i64,
+                                             _c_void_p]),
     "adaln_int4_quantize_weights": (ctypes.c_int, [_c_void_p, _i64, _i64, _i64, _c_void_p, _c_void_p, _c_void_p]),
     "adaln_int4_linear": (ctypes.c_int, [_c_void_p, _i64, _i64, _c_void_p, _c_void_p, _i64, _i64, _c_void_p,
                                          _c_void_p, _i64, _c_void_p]),
@@ -356,6 +359,29 @@ def orbit_qlinear_ws(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor
             _ptr(bias) if bias is not None else None, ORBIT_ACT_GELU if gelu else ORBIT_ACT_NONE,
             ORBIT_OUT_BF16 if out_dtype == torch.bfloat16 else ORBIT_OUT_F32, _ptr(out), max(out.stride(0), N),
             _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(x_codes)))
+    return out
+
+
+def orbit_qlinear_noalloc(cb_a: Codebook, x_codes: torch.Tensor, x_norm: torch.Tensor, cb_w: Codebook,
+                          w_codes: torch.Tensor, w_norm: torch.Tensor, bias: torch.Tensor = None, gelu: bool = False,
+                          out_dtype: torch.dtype = torch.float32, out: torch.Tensor = None) -> torch.Tensor:
+    """orbit_qlinear_ws with the K-split's partial sums in the library's own scratch array (32 MiB per
+    device): the C call allocates nothing.  Pass `out` to keep the binding from allocating the output.
+    Calls on one device must not overlap in time (they share the array)."""
+    M, N, K, dev = _qlinear_operands(cb_a, x_codes, x_norm, cb_w, w_codes, w_norm)
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype, device=dev)
+    _check_out(out, M, N, out_dtype, dev)
+    if bias is not None:
+        _expect(bias, "bias", torch.bfloat16, (N,), dev)
+    with torch.cuda.device(dev):
+        _check("orbit_qlinear_noalloc", lib().orbit_qlinear_noalloc(
+            cb_a.handle, _ptr(x_codes), _ptr(x_norm), M, cb_w.handle, _ptr(w_codes), _ptr(w_norm), N, K,
+            _ptr(bias) if bias is not None else None, ORBIT_ACT_GELU if gelu else ORBIT_ACT_NONE,
+            ORBIT_OUT_BF16 if out_dtype == torch.bfloat16 else ORBIT_OUT_F32, _ptr(out), max(out.stride(0), N),
+            _stream(x_codes)))
     return out
 
 

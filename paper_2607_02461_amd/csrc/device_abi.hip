@@ -95,6 +95,29 @@ orbit_status codebook_upload_dev(orbit_codebook c, int dev) {
     return ORBIT_OK;
 }
 
+// Scratch of the allocation-free layer (orbit_qlinear_noalloc): the K-split's fp32 partial sums
+// live in this file-scope device array instead of a caller workspace.  Every device that loads the
+// library holds its own copy until the process ends, and every call on a device shares it.  In host
+// code `scratch` names a host-side stand-in, not device memory: kernels get the address resolved
+// below, per device, and never the name itself.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+void* g_scratch[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+
+// The device address of `scratch` on device `dev` (the current device), looked up once per device.
+orbit_status scratch_on(int dev, void** out) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return ORBIT_OK;
+}
+
 // The current device, or -1 when no HIP device is visible (handles then stay host-only).
 orbit_status device_for_upload(int* dev) {
     int n = 0;
@@ -227,6 +250,10 @@ orbit_status orbit::upload_on_create(orbit_plan p, orbit_codebook c) {
     int dev;
     orbit_status st = device_for_upload(&dev);
     if (st != ORBIT_OK || dev < 0) return st;
+    // per-device set-up of the allocation-free layer's scratch address as well
+    void* sp = nullptr;
+    st = scratch_on(dev, &sp);
+    if (st != ORBIT_OK) return st;
     return p ? plan_upload_dev(p, dev) : codebook_upload_dev(c, dev);
 }
 
@@ -239,6 +266,9 @@ orbit_status rpbh_plan_upload(orbit_plan p) {
     DeviceInfo info;
     orbit_status st = current_device(&dev, &info);
     if (st != ORBIT_OK) return st;
+    void* sp = nullptr;
+    st = scratch_on(dev, &sp);
+    if (st != ORBIT_OK) return st;
     return plan_upload_dev(p, dev);
 }
 
@@ -248,6 +278,9 @@ orbit_status lloydmax_codebook_upload(orbit_codebook c) {
     int dev;
     DeviceInfo info;
     orbit_status st = current_device(&dev, &info);
+    if (st != ORBIT_OK) return st;
+    void* sp = nullptr;
+    st = scratch_on(dev, &sp);
     if (st != ORBIT_OK) return st;
     return codebook_upload_dev(c, dev);
 }
@@ -452,6 +485,35 @@ orbit_status orbit_qlinear_schedule(int64_t M, int64_t N, int64_t K, int64_t* ro
     int steps = 0;
     *splits = m_small > 0 ? lut_gemm_small_splits(m_small, N, K, info.cus, &steps) : 1;
     return ORBIT_OK;
+}
+
+orbit_status orbit_qlinear_noalloc(orbit_codebook cb_a, const uint8_t* x_codes, const float* x_norm, int64_t M,
+                                   orbit_codebook cb_w, const uint8_t* w_codes, const uint16_t* w_norm, int64_t N,
+                                   int64_t K, const uint16_t* bias, int32_t act, int32_t out_dtype, void* Y,
+                                   int64_t ldy, void* stream) {
+    clear_error();
+    // the split's partial sums must fit the scratch array; the other checks are orbit_qlinear_ws's
+    size_t need = 0;
+    if (M > 0 && N > 0 && K > 0 && K % 64 == 0 && K <= (int64_t)1 << 30) {
+        orbit_status st = orbit_qlinear_workspace_size(M, N, K, &need);
+        if (st != ORBIT_OK) return st;
+        if (need > kScratchBytes)
+            return fail(ORBIT_EUNSUPPORTED,
+                        "orbit_qlinear_noalloc: a %lld x %lld x %lld layer splits over K into %zu bytes of partial sums, "
+                        "above the %zu-byte scratch limit (use orbit_qlinear_ws with a workspace of that size)",
+                        (long long)M, (long long)N, (long long)K, need, kScratchBytes);
+    }
+    void* ws = nullptr;
+    if (need > 0) {
+        int dev;
+        DeviceInfo info;
+        orbit_status st = current_device(&dev, &info);
+        if (st != ORBIT_OK) return st;
+        st = scratch_on(dev, &ws);
+        if (st != ORBIT_OK) return st;
+    }
+    return orbit_qlinear_ws(cb_a, x_codes, x_norm, M, cb_w, w_codes, w_norm, N, K, bias, act, out_dtype, Y, ldy, ws,
+                            ws ? kScratchBytes : 0, stream);
 }
 
 }  // extern "C"
