@@ -47,6 +47,18 @@ def parse():
                          "counter profile of this run holds a kernel of known traffic to scale by")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-kernel HBM bytes measured with rocprofv3 counters (optional)")
+    ap.add_argument("--part-reps", type=int, default=10,
+                    help="timed launches of each layer kernel on its own (the roofline's per-kernel times)")
+    ap.add_argument("--config-reps", type=int, default=10,
+                    help="timed launches per linear of the other workloads' configurations (0 skips them)")
+    ap.add_argument("--image-reps", type=int, default=10,
+                    help="timed launches per shape of the per-image rotation cost (0 skips it)")
+    ap.add_argument("--cpu-one-thread-rows", type=int, default=1536,
+                    help="token rows of the oracle's single-thread CPU sample (0 disables it)")
+    ap.add_argument("--extras", type=int, default=1,
+                    help="0 skips the entries after the step (block-size rule, rotation classes, fused "
+                         "epilogue, MLP chain, W4A6), e.g. for counter profiles of the step alone")
+    ap.add_argument("--cpu-baseline-worker", default=None, help=argparse.SUPPRESS)
     return ap.parse_args()
 
 
@@ -67,6 +79,9 @@ def quant_bytes(M, K, bits):
 
 def main():
     args = parse()
+    if args.cpu_baseline_worker:
+        cpu_baseline_worker(args.cpu_baseline_worker)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1 "
                                    "(rows shard across GPUs with no exchange, see the design notes)"}))
@@ -129,13 +144,24 @@ def main():
     weight_pass_ms = ws.elapsed_time(we) / wp_reps
     weight_bytes = sum(L["lin"].N * (2 * L["lin"].K + L["lin"].K * L["lin"].bw // 8 + 2) for L in layers)
 
-    if args.copy_calibration_mib > 0:
-        n = args.copy_calibration_mib << 20
-        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
+    # a plain device-to-device copy: the attainable HBM rate beside the 8 TB/s peak, and (with
+    # --copy-calibration-mib) a kernel of known traffic in counter profiles of this run
+    copy_mib = args.copy_calibration_mib if args.copy_calibration_mib > 0 else 1024
+    src = torch.empty(copy_mib << 20, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record()
+    for _ in range(5):
         dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    c1.record()
+    torch.cuda.synchronize()
+    copy_ms = c0.elapsed_time(c1) / 5
+    hbm_copy = {"bytes_read_plus_written": 2 * (copy_mib << 20), "ms": copy_ms,
+                "gbs": 2 * (copy_mib << 20) / (copy_ms * 1e-3) / 1e9,
+                "frac_of_hbm": 2 * (copy_mib << 20) / (copy_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    del src, dst
 
     # ---- the step --------------------------------------------------------------------------
     nl = len(layers)
@@ -188,35 +214,139 @@ def main():
         except (OSError, ValueError):
             traffic = None
 
-    gemm_launch_flops = float(flops.mean())
-    gemm_avg_ms = float(gemm_ms.mean())
+    # The layer's kernels, each launch timed alone with HIP events on the stream it runs on: the
+    # rows the 256x256 kernel takes and the rows the 128x128 kernel takes (split over K with the
+    # workspace, then the reduction), as orbit_qlinear_schedule names them
+    parts = [p for L in layers for p in gemm_parts(oq, L, args.part_reps)]
+    dom = [p for p in parts if p["kernel"].startswith("lut_gemm_big")]
+    if not dom:   # a layer too small for the large kernel (c1): its split kernel pair dominates
+        dom = parts
+    dom_flops = sum(p["flops"] for p in dom)
+    dom_ms = sum(p["ms"] for p in dom)
     roofline = {
-        "kernel": "lut_gemm_big" if wl is workloads.C4 else (
-            "lut_gemm_kernel+lut_gemm_reduce" if layers[0]["ws"].numel() > 16 else "lut_gemm_kernel"),
-        # c4's down-projection: lut_gemm_big on the rows of its full rounds, then the other rows
-        # on the 128x128 kernel split over K (the workspace) and lut_gemm_reduce
-        "workspace_bytes": [oq.orbit_qlinear_workspace_size(L["lin"].M, L["lin"].N, L["lin"].K) for L in layers],
+        "kernel": dom[0]["kernel"],
         "bound": "mfma",
-        "achieved": gemm_launch_flops / (gemm_avg_ms * 1e-3) / 1e12,
+        "achieved": dom_flops / (dom_ms * 1e-3) / 1e12,
         "peak": FP16_MFMA_PEAK_TFLOPS,
         "unit": "TFLOP/s",
-        "frac": gemm_launch_flops / (gemm_avg_ms * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS,
+        "frac": dom_flops / (dom_ms * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS,
         "traffic": (traffic or {}).get("gemm_bytes_per_launch"),
-        "avg_launch_ms": gemm_avg_ms,
-        "algorithmic_flops_per_launch": gemm_launch_flops,
+        "achieved_is": "2*rows*N*K of each launch of this kernel in the step / its HIP-event launch time, "
+                       "over the launches listed in 'launches'",
+        "launches": [p for p in parts if p["kernel"] == dom[0]["kernel"]],
+        "other_launches": [p for p in parts if p["kernel"] != dom[0]["kernel"]],
+        "call_ms_in_step": [float(v) for v in gemm_ms],
+        "workspace_bytes": [oq.orbit_qlinear_workspace_size(L["lin"].M, L["lin"].N, L["lin"].K) for L in layers],
     }
+    qkern = [f"rpbh_quantize_kernel<{L['lin'].ba},false,{'true' if L['lin'].h > 128 else 'false'},true>"
+             for L in layers]
     roofline_q = {
-        "kernel": "rpbh_quantize_kernel",
+        "kernel": qkern[0] if len(set(qkern)) == 1 else qkern,
         "bound": "hbm",
         "achieved": quant_gbs,
         "peak": HBM_PEAK_GBS,
         "unit": "GB/s",
         "frac": quant_gbs / HBM_PEAK_GBS,
         "traffic": (traffic or {}).get("quant_bytes_per_launch"),
-        "avg_launch_ms": [float(v) for v in quant_ms],
-        "algorithmic_bytes_per_launch": [float(v) for v in qbytes],
+        "launches": [{"linear": L["lin"].name, "M": L["lin"].M, "K": L["lin"].K, "bits": L["lin"].ba,
+                      "ms": float(quant_ms[i]), "algorithmic_bytes": float(qbytes[i]),
+                      "gbs": float(qbytes[i]) / (float(quant_ms[i]) * 1e-3) / 1e9,
+                      "frac": float(qbytes[i]) / (float(quant_ms[i]) * 1e-3) / 1e9 / HBM_PEAK_GBS}
+                     for i, L in enumerate(layers)],
+        "attainable_copy_gbs": hbm_copy["gbs"],
     }
 
+    paper_h = rot = fused = chain = a6 = None
+    if args.extras:
+        paper_h, rot, fused, chain, a6 = extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms)
+
+    configs = None
+    if args.config_reps > 0:
+        configs = configs_sweep(oq, workloads, dev, args.config_reps)
+
+    per_image = None
+    if args.image_reps > 0:
+        per_image = rotation_per_image(oq, dev, args.image_reps)
+
+    adaln = None
+    if args.adaln_steps > 0:
+        adaln = adaln_sweep(oq, workloads, dev, args.adaln_steps)
+
+    trunk = None
+    if args.trunk_steps > 0:
+        trunk = trunk_sweep(oq, workloads, dev, args.trunk_steps)
+
+    cpu = None
+    if args.cpu_baseline_rows > 0:
+        step()                     # the step's own outputs back in place (later entries reused buffers)
+        torch.cuda.synchronize()
+        cpu = cpu_baseline(layers, args.cpu_baseline_rows, one_thread_rows=args.cpu_one_thread_rows, parity=True)
+
+    out = {
+        "metric": METRIC,
+        "value": step_tflops,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "description": wl.description,
+            "linears": [{"name": L["lin"].name, "M": L["lin"].M, "K": L["lin"].K, "N": L["lin"].N,
+                         "bits": f"W{L['lin'].bw}A{L['lin'].ba}", "h": L["lin"].h} for L in layers],
+            "value_is": "GEMM flops of the step / step time (quantizer + GEMM per linear)",
+            "arith": "quantizer fp32; GEMM fp16 MFMA operands, fp32 accumulate",
+            # inputs above the 256 MB Infinity Cache stream from HBM on every step
+            "cache": "cold" if min(L["X"].numel() * 2 for L in layers) > (256 << 20) else "warm",
+        },
+        "components": {
+            "orbit_qlinear_tflops": gemm_tflops,
+            "orbit_qlinear_frac_of_fp16_peak": gemm_tflops / FP16_MFMA_PEAK_TFLOPS,
+            "rpbh_quantize_act_gbs": quant_gbs,
+            "rpbh_quantize_act_frac_of_hbm": quant_gbs / HBM_PEAK_GBS,
+            "quant_ms": [float(v) for v in quant_ms],
+            "gemm_ms": [float(v) for v in gemm_ms],
+            "quant_ms_median": [float(v) for v in np.median(q_all, axis=0)],
+            "quant_ms_min": [float(v) for v in q_all.min(axis=0)],
+            "gemm_ms_median": [float(v) for v in np.median(g_all, axis=0)],
+            "gemm_ms_min": [float(v) for v in g_all.min(axis=0)],
+            "weight_pass_ms": weight_pass_ms,
+            "weight_pass_gbs": weight_bytes / (weight_pass_ms * 1e-3) / 1e9,
+            "host_plan_codebook_s": host_offline_s,
+            "wall_s_timed_region": wall_s,
+        },
+        "roofline": roofline,
+        "roofline_quantizer": roofline_q,
+        "hbm_copy": hbm_copy,
+        "parity": (cpu or {}).pop("parity", None),
+        "configs": configs,
+        "rotation_per_image": per_image,
+        "quantizer_paper_block_rule": paper_h,
+        "rotation_classes": rot,
+        "fused_epilogue": fused,
+        "mlp_chain": chain,
+        "w4a6": a6,
+        "trunk_c5": trunk,
+        "adaln_int4": adaln,
+        "cpu_baseline": cpu,
+        "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0),
+                "host_cpu_count": os.cpu_count(),
+                "arch": torch.cuda.get_device_properties(0).gcnArchName,
+                "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,
+                "memory_gib": torch.cuda.get_device_properties(0).total_memory / 2 ** 30},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
+    """The entries after the step: the paper's block-size rule, the rotation classes, the fused
+    epilogue, the MLP chain and the W4A6 recipe, each timed on the step's own inputs."""
     # NEXT row: the activation quantizer with the paper's block-size rule (largest power of two
     # dividing d: 1024 for 5120, 512 for 13824), same inputs, timed alone
     paper_h = {}
@@ -379,73 +509,162 @@ def main():
           "gemm_ms": g6_ms, "gemm_tflops": float(flops[0]) / (g6_ms * 1e-3) / 1e12}
     del xc6
 
-    adaln = None
-    if args.adaln_steps > 0:
-        adaln = adaln_sweep(oq, workloads, dev, args.adaln_steps)
+    return paper_h, rot, fused, chain, a6
 
-    trunk = None
-    if args.trunk_steps > 0:
-        trunk = trunk_sweep(oq, workloads, dev, args.trunk_steps)
 
-    cpu = None
-    if args.cpu_baseline_rows > 0:
-        cpu = cpu_baseline(layers, args.cpu_baseline_rows)
+def _timed(fn, reps, before=None):
+    """Mean, median and minimum of `reps` launches of fn, each bracketed by its own HIP events on the
+    current stream; `before` (untimed) runs ahead of each launch."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    fn()
+    torch.cuda.synchronize()
+    for e0, e1 in ev:
+        if before is not None:
+            before()
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    t = np.array([e0.elapsed_time(e1) for e0, e1 in ev])
+    return float(t.mean()), float(np.median(t)), float(t.min())
 
-    out = {
-        "metric": METRIC,
-        "value": step_tflops,
-        "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f16",
-        "data": "synthetic",
-        "config": {
-            "workload": wl.name,
-            "description": wl.description,
-            "linears": [{"name": L["lin"].name, "M": L["lin"].M, "K": L["lin"].K, "N": L["lin"].N,
-                         "bits": f"W{L['lin'].bw}A{L['lin'].ba}", "h": L["lin"].h} for L in layers],
-            "value_is": "GEMM flops of the step / step time (quantizer + GEMM per linear)",
-            "arith": "quantizer fp32; GEMM fp16 MFMA operands, fp32 accumulate",
-            # inputs above the 256 MB Infinity Cache stream from HBM on every step
-            "cache": "cold" if min(L["X"].numel() * 2 for L in layers) > (256 << 20) else "warm",
-        },
-        "components": {
-            "orbit_qlinear_tflops": gemm_tflops,
-            "orbit_qlinear_frac_of_fp16_peak": gemm_tflops / FP16_MFMA_PEAK_TFLOPS,
-            "rpbh_quantize_act_gbs": quant_gbs,
-            "rpbh_quantize_act_frac_of_hbm": quant_gbs / HBM_PEAK_GBS,
-            "quant_ms": [float(v) for v in quant_ms],
-            "gemm_ms": [float(v) for v in gemm_ms],
-            "quant_ms_median": [float(v) for v in np.median(q_all, axis=0)],
-            "quant_ms_min": [float(v) for v in q_all.min(axis=0)],
-            "gemm_ms_median": [float(v) for v in np.median(g_all, axis=0)],
-            "gemm_ms_min": [float(v) for v in g_all.min(axis=0)],
-            "weight_pass_ms": weight_pass_ms,
-            "weight_pass_gbs": weight_bytes / (weight_pass_ms * 1e-3) / 1e9,
-            "host_plan_codebook_s": host_offline_s,
-            "wall_s_timed_region": wall_s,
-        },
-        "roofline": roofline,
-        "roofline_quantizer": roofline_q,
-        "quantizer_paper_block_rule": paper_h,
-        "rotation_classes": rot,
-        "fused_epilogue": fused,
-        "mlp_chain": chain,
-        "w4a6": a6,
-        "trunk_c5": trunk,
-        "adaln_int4": adaln,
-        "cpu_baseline": cpu,
-        "env": {"torch": torch.__version__, "hip": torch.version.hip, "device": torch.cuda.get_device_name(0),
-                "arch": torch.cuda.get_device_properties(0).gcnArchName,
-                "compute_units": torch.cuda.get_device_properties(0).multi_processor_count,
-                "memory_gib": torch.cuda.get_device_properties(0).total_memory / 2 ** 30},
-    }
-    print(json.dumps(out), flush=True)
+
+def gemm_parts(oq, L, reps):
+    """The kernel launches of one layer call, each timed alone: rows [0, rows_large) on the 256x256
+    kernel, then rows [rows_large, M) on the 128x128 kernel, split over K with the layer's workspace
+    and followed by the reduction when the schedule splits them.  Each part is the same launch the
+    whole call makes (the same rows, operands and split)."""
+    lin = L["lin"]
+    M, N, K = lin.M, lin.N, lin.K
+    rows, splits = oq.orbit_qlinear_schedule(M, N, K)
+    out = []
+    for r0, r1 in ((0, rows), (rows, M)):
+        if r1 <= r0:
+            continue
+        xc, xn, Y = L["xc"][r0:r1], L["xn"][r0:r1], L["Y"][r0:r1]
+        big = r0 == 0 and rows > 0
+
+        def call():
+            oq.orbit_qlinear_ws(L["cba"], xc, xn, L["cbw"], L["wc"], L["wn"], L["ws"], out=Y)
+
+        mean, med, mn = _timed(call, reps)
+        fl = 2.0 * (r1 - r0) * N * K
+        name = (f"lut_gemm_big<{lin.ba},{lin.bw}>" if big else
+                f"lut_gemm_kernel<{lin.ba},{lin.bw},{'true' if splits > 1 else 'false'}>"
+                + ("+lut_gemm_reduce" if splits > 1 else ""))
+        out.append({"linear": lin.name, "kernel": name, "rows": [r0, r1], "N": N, "K": K, "splits": 1 if big else splits,
+                    "flops": fl, "ms": mean, "ms_median": med, "ms_min": mn,
+                    "tflops": fl / (mean * 1e-3) / 1e12, "frac": fl / (mean * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS})
+    return out
+
+
+def configs_sweep(oq, workloads, dev, reps):
+    """Every linear of the other workload configurations at its bit pair, the quantizer and the layer
+    each timed launch by launch: the single layer (c1), the image-DiT MLP at W4A4 and W3A4 (c2,
+    timestep 0), the image-DiT attention projections at W2A4 and W3A3 (c3), and the video recipe's
+    W4A6 on the c4 up-projection.  Inputs smaller than the 256 MB Infinity Cache are evicted before
+    each timed launch by writing a 512 MB buffer, so every launch streams its operands from HBM."""
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+
+    def evict():
+        flush.fill_(0)
+
+    jobs = []
+    X1, W1 = workloads.c1_inputs(device=dev)
+    jobs.append(("c1_single_w4a4", workloads.C1.linears[0], X1, W1, workloads.C1.plan_seed))
+    Xu, Xd = workloads.c2_up_acts(0, device=dev), workloads.c2_down_acts(0, device=dev)
+    Wu, Wd = workloads.c2_weights(device=dev)
+    for lin in workloads.C2.linears:
+        X, W = (Xu, Wu) if lin.name.startswith("up") else (Xd, Wd)
+        jobs.append(("c2_image_mlp", lin, X, W, workloads.C2.plan_seed))
+    Xq, Xo, Wq, Wo = workloads.c3_inputs(device=dev)
+    for lin in workloads.C3.linears:
+        X, W = (Xq, Wq) if lin.name.startswith("qkv") else (Xo, Wo)
+        jobs.append(("c3_image_attn", lin, X, W, workloads.C3.plan_seed))
+    fr, tpf, txt = workloads.C4.extra["frames"], workloads.C4.extra["tokens_per_frame"], workloads.C4.extra["text_tokens"]
+    up = workloads.C4.linears[0]
+    X4 = workloads.video_acts(fr * tpf, txt, up.K, 4, fr, workloads.C4.data_seed, 0, device=dev)
+    W4 = workloads.gaussian_weights(up.N, up.K, 0.015, workloads.C4.data_seed, 0, device=dev)
+    jobs.append(("c4_video_mlp_w4a6", workloads.Linear("up_w4a6", up.M, up.K, up.N, 4, 6), X4, W4,
+                 workloads.C4.plan_seed))
+
+    res = []
+    for wname, lin, X, W, seed in jobs:
+        plan = oq.rpbh_plan(lin.K, lin.h, seed)
+        cba, cbw = oq.lloydmax_codebook(lin.ba, lin.K), oq.lloydmax_codebook(lin.bw, lin.K)
+        wc, wn = oq.quantize_weights_offline(plan, cbw, W)
+        xc = torch.empty((lin.M, lin.K * lin.ba // 8), dtype=torch.uint8, device=dev)
+        xn = torch.empty((lin.M,), dtype=torch.float32, device=dev)
+        Y = torch.empty((lin.M, lin.N), dtype=torch.float32, device=dev)
+        ws = torch.empty(max(16, oq.orbit_qlinear_workspace_size(lin.M, lin.N, lin.K)), dtype=torch.uint8, device=dev)
+        cold = X.numel() * 2 > (256 << 20)
+        q = _timed(lambda: oq.rpbh_quantize_act(plan, cba, X, 1e-10, xc, xn), reps, None if cold else evict)
+        g = _timed(lambda: oq.orbit_qlinear_ws(cba, xc, xn, cbw, wc, wn, ws, out=Y), reps, evict)
+        qb = quant_bytes(lin.M, lin.K, lin.ba)
+        fl = 2.0 * lin.M * lin.N * lin.K
+        rows, splits = oq.orbit_qlinear_schedule(lin.M, lin.N, lin.K)
+        res.append({"workload": wname, "linear": lin.name, "M": lin.M, "K": lin.K, "N": lin.N,
+                    "bits": f"W{lin.bw}A{lin.ba}", "h": lin.h, "schedule": {"rows_large": rows, "splits": splits},
+                    "quant_ms": q[0], "quant_ms_min": q[2], "quant_gbs": qb / (q[0] * 1e-3) / 1e9,
+                    "quant_frac_of_hbm": qb / (q[0] * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                    "gemm_ms": g[0], "gemm_ms_min": g[2], "gemm_tflops": fl / (g[0] * 1e-3) / 1e12,
+                    "gemm_frac_of_fp16_peak": fl / (g[0] * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS})
+        del wc, wn, xc, xn, Y, ws
+    del flush
+    return {"cache": "cold: operands below 256 MB evicted before every timed launch", "linears": res}
+
+
+# FLUX.1-shaped image DiT at 1024^2 (hidden 3072, MLP 12288): the activation inputs the quantized
+# projections read per denoising step, as (tokens, d, count).  Each of the 19 double-stream blocks
+# has an image stream (4096 tokens) and a text stream (512 tokens), each reading three inputs of
+# width 3072 (attention QKV, attention output, FFN up) and one of 12288 (FFN down); each of the 38
+# single-stream blocks (4608 tokens) reads one of 3072 (its fused QKV and FFN up) and one of
+# 3072 + 12288 = 15360 (its fused output projection).  4 steps per image (the schnell sampler).
+FLUX_ROTATION_INPUTS = ((4096, 3072, 19 * 3), (4096, 12288, 19), (512, 3072, 19 * 3), (512, 12288, 19),
+                        (4608, 3072, 38), (4608, 15360, 38))
+FLUX_STEPS = 4
+# the paper's per-image activation-rotation latency on one H100 (FLUX.1-schnell, 1024^2), seconds
+PAPER_H100_ROTATION_S = {"rpbh": 0.451, "block_rht": 0.381, "full_rht": 0.452, "dense_haar": 11.65}
+
+
+def rotation_per_image(oq, dev, reps):
+    """Analogue of the paper's per-image activation-rotation latency (FLUX.1-schnell at 1024^2, all
+    quantized layers and steps): for each rotation class, the fused quantizer (rotation, norm, 4-bit
+    encode) timed once per input shape, times how often a step reads that shape, times 4 steps.
+    Dense Haar is the rotation alone, a bf16 GEMM X Q^T with a d x d matrix (a random one: the GEMM's
+    time does not depend on Q being orthogonal).  Inputs are synthetic N(0, 1) rows, timed back to
+    back (warm: in a model each input was just written by the previous layer)."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    per_shape, tot = [], {"rpbh_h128": 0.0, "rpbh_paper_rule": 0.0, "block_rht_h128": 0.0,
+                          "block_rht_paper_rule": 0.0, "dense_haar": 0.0}
+    for M, d, count in FLUX_ROTATION_INPUTS:
+        X = torch.randn((M, d), generator=g, device=dev).to(torch.bfloat16)
+        cb = oq.lloydmax_codebook(4, d)
+        xc = torch.empty((M, d // 2), dtype=torch.uint8, device=dev)
+        xn = torch.empty((M,), dtype=torch.float32, device=dev)
+        row = {"M": M, "d": d, "per_step": count}
+        for hh, tag in ((128, "h128"), (0, "paper_rule")):
+            pr = oq.rpbh_plan(d, hh, 0)
+            _, signs = pr.arrays()
+            pb = oq.rpbh_plan_from_arrays(d, pr.h, np.arange(d), signs)
+            for name, plan in (("rpbh", pr), ("block_rht", pb)):
+                ms = _timed(lambda: oq.rpbh_quantize_act(plan, cb, X, 1e-10, xc, xn), reps)[0]
+                row[f"{name}_{tag}_ms"] = ms
+                row[f"{name}_{tag}_h"] = pr.h
+                tot[f"{name}_{tag}"] += ms * count * FLUX_STEPS
+        Q = (torch.randn((d, d), generator=g, device=dev) / d ** 0.5).to(torch.bfloat16)
+        Xr = torch.empty((M, d), dtype=torch.bfloat16, device=dev)
+        ms = _timed(lambda: torch.matmul(X, Q, out=Xr), max(3, reps // 2))[0]
+        row["dense_haar_ms"] = ms
+        tot["dense_haar"] += ms * count * FLUX_STEPS
+        per_shape.append(row)
+        del X, xc, xn, Q, Xr
+    return {"model": "FLUX.1-shaped image DiT, 1024^2, 4 steps, 4608 tokens (4096 image + 512 text)",
+            "seconds_per_image": {k: v * 1e-3 for k, v in tot.items()},
+            "quantizer_includes": "rotation + norm + 4-bit Lloyd-Max encode and pack (the fused kernel)",
+            "paper_h100_rotation_only_s": PAPER_H100_ROTATION_S,
+            "shapes": per_shape}
 
 
 def trunk_sweep(oq, workloads, dev, steps, warmup=1):
@@ -599,43 +818,160 @@ def adaln_sweep(oq, workloads, dev, steps, warmup=2):
     return out
 
 
-def cpu_baseline(layers, rows, min_seconds=10.0):
-    """The fp64 oracle timed on the host cores on a bounded sample: `rows` token rows through
-    every linear of the step (quantize + contraction).  The oracle's weight codes are made
-    once, outside the timing, as the GPU's offline weight pass is outside the step."""
-    import oracle
+def _blas_threads():
     try:
         from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        blas_threads = os.cpu_count()
+        return os.cpu_count()
+
+
+def _oracle_pass(oracle, prepared, rows, min_seconds):
+    """Oracle work on the host: every prepared linear's rows quantized and contracted in fp64, passes
+    repeated until `rows` rows and at least `min_seconds` are done.  Returns (flops, seconds, passes,
+    the last pass's activation codes per linear)."""
+    t0 = time.perf_counter()
+    flops, done, passes, last = 0.0, 0, 0, []
+    while done < rows or time.perf_counter() - t0 < min_seconds:
+        last = []
+        for lin, plan, cba, cbw, cw, r, X in prepared:
+            cx, s, U = oracle.quantize_act(X, plan, cba)
+            oracle.qlinear(cx, s, cba.levels, cw, r, cbw.levels)
+            flops += 2.0 * X.shape[0] * lin.N * lin.K
+            last.append((cx, s, U))
+        done += prepared[0][6].shape[0]
+        passes += 1
+    return flops, time.perf_counter() - t0, passes, last
+
+
+def cpu_baseline(layers, rows, min_seconds=10.0, one_thread_rows=0, parity=False):
+    """The fp64 oracle timed on the host cores on a bounded sample: `rows` token rows through
+    every linear of the step (quantize + contraction), with the BLAS library's own thread count, and
+    (one_thread_rows > 0) a smaller sample in a child process limited to one thread.  The oracle's
+    weight codes are made once, outside the timing, as the GPU's offline weight pass is outside the
+    step.  With parity=True the same oracle results are compared with the GPU's outputs of the step
+    (activation and weight codes, norms, and 256 output rows against the oracle contraction of the
+    GPU's own codes); the counts go to a 'parity' entry."""
+    import oracle
     prepared = []
     for L in layers:
         lin = L["lin"]
         plan = oracle.rpbh_plan(lin.K, lin.h, 0)
         cba, cbw = oracle.lloydmax_codebook(lin.ba, lin.K), oracle.lloydmax_codebook(lin.bw, lin.K)
         W = L["W"].float().cpu().numpy().astype(np.float64)
-        cw, r, _ = oracle.quantize_weights(W, plan, cbw)
+        cw, r, Uw = oracle.quantize_weights(W, plan, cbw)
         del W
         X = L["X"][:rows].float().cpu().numpy().astype(np.float64)
         prepared.append((lin, plan, cba, cbw, cw, r, X))
+        L["_oracle_w"] = (cw, r, Uw) if parity else None
     # a workload with fewer rows than the sample asks for (c1: 256) repeats its rows, and passes
     # continue until at least min_seconds of work, so that the rate is not a timer artefact
-    t0 = time.perf_counter()
-    flops, done, passes = 0.0, 0, 0
-    while done < rows or time.perf_counter() - t0 < min_seconds:
-        for lin, plan, cba, cbw, cw, r, X in prepared:
-            cx, s, _ = oracle.quantize_act(X, plan, cba)
-            oracle.qlinear(cx, s, cba.levels, cw, r, cbw.levels)
-            flops += 2.0 * X.shape[0] * lin.N * lin.K
-        done += prepared[0][6].shape[0]
-        passes += 1
-    dt = time.perf_counter() - t0
+    flops, dt, passes, last = _oracle_pass(oracle, prepared, rows, min_seconds)
     n = prepared[0][6].shape[0]
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": blas_threads, "kind": "oracle",
-            "sample": f"{n} token rows through every linear of the step (quantize + fp64 contraction), "
-                      f"{passes} pass{'es' if passes > 1 else ''}, {dt:.1f} s; same metric unit as the GPU value",
-            "seconds": dt}
+    out = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": _blas_threads(), "kind": "oracle",
+           "host_cpu_count": os.cpu_count(),
+           "sample": f"{n} token rows through every linear of the step (quantize + fp64 contraction), "
+                     f"{passes} pass{'es' if passes > 1 else ''}, {dt:.1f} s, BLAS threads as the library "
+                     f"chose; same metric unit as the GPU value",
+           "seconds": dt}
+    if one_thread_rows > 0:
+        out["one_thread"] = cpu_baseline_one_thread(prepared, one_thread_rows, min_seconds)
+    if parity:
+        out["parity"] = parity_vs_oracle(oracle, layers, prepared, last)
+    return out
+
+
+def parity_vs_oracle(oracle, layers, prepared, last, gemm_rows=256, band=1e-5):
+    """The GPU's outputs of the step against the oracle on the baseline's sample: codes equal off
+    near-ties (|u - tau| > 1e-5); within a near-tie only the two codes across the nearest threshold are
+    nearest centroids (Eq. (3) ties there), so other codes count as invalid.  Norms to 1e-5 (s) and
+    one bf16 ulp (r').  The layer on gemm_rows rows against the fp64 contraction of the GPU's own codes,
+    norms and fp16 levels: relative Frobenius error and the worst element over the per-element bar
+    1e-4 s_n r'_i ||a_n|| ||b_i||."""
+    res = []
+    for L, (lin, plan, cba, cbw, cw, r, X), (cx, s, Ux) in zip(layers, prepared, last):
+        n = X.shape[0]
+        gx = oracle.unpack_codes(L["xc"][:n].cpu().numpy(), lin.ba, lin.K)
+        gw = oracle.unpack_codes(L["wc"].cpu().numpy(), lin.bw, lin.K)
+        _, _, Uw = L.pop("_oracle_w")
+        entry = {"linear": lin.name, "act_rows": n, "weight_rows": lin.N}
+        for tag, g, c, U, th in (("act", gx, cx, Ux, cba.thresholds), ("weights", gw, cw, Uw, cbw.thresholds)):
+            near = oracle.near_tie_mask(U, th, band)
+            j = oracle.nearest_threshold(U, th)
+            mism = g != c
+            entry[tag] = {"codes": int(g.size), "near_ties": int(near.sum()),
+                          "near_tie_mismatches": int(np.sum(mism & near)),
+                          "near_tie_invalid": int(np.sum(mism & near & (g != j) & (g != j + 1))),
+                          "mismatches_off_tie": int(np.sum(mism & ~near))}
+        gs = L["xn"][:n].cpu().numpy().astype(np.float64)
+        gr = L["wn"].float().cpu().numpy().astype(np.float64)
+        ulp = np.ldexp(1.0, np.frexp(np.maximum(r, 1e-30))[1] - 8)
+        entry["s_max_rel_err"] = float(np.max(np.abs(gs - s) / np.maximum(s, 1e-30)))
+        entry["r_max_err_bf16_ulps"] = float(np.max(np.abs(gr - r) / ulp))
+        m = min(gemm_rows, n)
+        la, lw = oracle.fp16_round(cba.levels), oracle.fp16_round(cbw.levels)
+        ref = oracle.qlinear(gx[:m], gs[:m], la, gw, gr, lw)
+        Y = L["Y"][:m].double().cpu().numpy()
+        unit = (gs[:m] * np.linalg.norm(la[gx[:m]], axis=1))[:, None] * (gr * np.linalg.norm(lw[gw], axis=1))[None, :]
+        entry["gemm_rows"] = m
+        entry["gemm_rel_f"] = float(np.linalg.norm(Y - ref) / np.linalg.norm(ref))
+        entry["gemm_worst_elem_over_bar"] = float(np.max(np.abs(Y - ref) / np.maximum(1e-4 * unit, 1e-300)))
+        res.append(entry)
+    ok = all(e[t]["mismatches_off_tie"] == 0 and e[t]["near_tie_invalid"] == 0 for e in res for t in ("act", "weights"))
+    ok = ok and all(e["s_max_rel_err"] <= 1e-5 and e["r_max_err_bf16_ulps"] <= 1.0 and e["gemm_rel_f"] <= 2e-3
+                    and e["gemm_worst_elem_over_bar"] <= 1.0 for e in res)
+    return {"passed": bool(ok), "band": band, "linears": res}
+
+
+def cpu_baseline_one_thread(prepared, rows, min_seconds):
+    """The same oracle work in a child process with every BLAS/OpenMP pool at one thread, on the
+    first `rows` rows of the sample (the pools are sized when numpy loads, so it takes a process of
+    its own)."""
+    import subprocess
+    import tempfile
+    tmp = tempfile.mkdtemp(prefix="orbit_cpu1_")
+    path = os.path.join(tmp, "sample.npz")
+    arrays = {}
+    for i, (lin, plan, cba, cbw, cw, r, X) in enumerate(prepared):
+        arrays[f"X{i}"] = X[:rows]
+        arrays[f"cw{i}"] = cw.astype(np.uint8)
+        arrays[f"r{i}"] = r
+        arrays[f"shape{i}"] = np.array([lin.M, lin.K, lin.N, lin.bw, lin.ba, lin.h], dtype=np.int64)
+    arrays["min_seconds"] = np.array([min_seconds])
+    np.savez(path, **arrays)
+    env = dict(os.environ)
+    for v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS", "BLIS_NUM_THREADS"):
+        env[v] = "1"
+    try:
+        r = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-baseline-worker", path],
+                           capture_output=True, text=True, env=env, timeout=600)
+        line = [l for l in r.stdout.splitlines() if l.startswith("{")]
+        res = json.loads(line[-1]) if r.returncode == 0 and line else {"error": r.stderr[-500:]}
+    finally:
+        for f in os.listdir(tmp):
+            os.remove(os.path.join(tmp, f))
+        os.rmdir(tmp)
+    return res
+
+
+def cpu_baseline_worker(path):
+    """Child process of cpu_baseline_one_thread: times the oracle on the saved sample, prints JSON."""
+    import oracle
+    z = np.load(path)
+    prepared, i = [], 0
+    while f"X{i}" in z:
+        M, K, N, bw, ba, h = (int(v) for v in z[f"shape{i}"])
+        from paper_2607_02461_amd.workloads import Linear
+        lin = Linear(f"linear{i}", M, K, N, bw, ba, h)
+        prepared.append((lin, oracle.rpbh_plan(K, h, 0), oracle.lloydmax_codebook(ba, K),
+                         oracle.lloydmax_codebook(bw, K), z[f"cw{i}"].astype(np.int64), z[f"r{i}"], z[f"X{i}"]))
+        i += 1
+    rows = prepared[0][6].shape[0]
+    flops, dt, passes, _ = _oracle_pass(oracle, prepared, rows, float(z["min_seconds"][0]))
+    print(json.dumps({"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": _blas_threads(), "kind": "oracle",
+                      "sample": f"{rows} token rows through every linear of the step (quantize + fp64 contraction), "
+                                f"{passes} pass{'es' if passes > 1 else ''}, {dt:.1f} s, one thread",
+                      "seconds": dt}), flush=True)
 
 
 if __name__ == "__main__":
