@@ -19,7 +19,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
-SOURCES = ["host.cpp", "device_abi.hip", "rpbh_quantize.hip", "lut_gemm.hip", "adaln_rtn.hip"]
+SOURCES = ["host.cpp", "device_abi.hip", "rpbh_quantize.hip", "rpbh_quantize_row.hip", "lut_gemm.hip", "adaln_rtn.hip"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function", "-I", os.path.join(ROOT, "include")]
 # packed fp32 ops stay off on the device (the host pass ignores the feature with a warning)

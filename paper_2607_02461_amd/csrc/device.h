@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <mutex>
 
 namespace orbit {
 
@@ -19,6 +20,27 @@ inline hipError_t raise_lds_limit(const void* kernel, int bytes, std::atomic<uin
     e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e == hipSuccess) done.fetch_or(bit, std::memory_order_acq_rel);
     return e;
+}
+
+// Workgroups of `kernel` resident on one compute unit at `threads` threads and `smem` bytes of
+// dynamic LDS (registers, LDS and wave slots together), looked up once per shape.
+inline int resident_blocks(const void* kernel, int threads, size_t smem) {
+    struct Entry {
+        const void* k;
+        int t;
+        size_t s;
+        int n;
+    };
+    static std::mutex mu;
+    static Entry cache[64];
+    static int used = 0;
+    std::lock_guard<std::mutex> lk(mu);
+    for (int i = 0; i < used; ++i)
+        if (cache[i].k == kernel && cache[i].t == threads && cache[i].s == smem) return cache[i].n;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, smem) != hipSuccess || n < 1) n = 1;
+    if (used < 64) cache[used++] = Entry{kernel, threads, smem, n};
+    return n;
 }
 
 // Fused RPBH quantizer (activations: fp32 norms; weights: bf16 norms).
@@ -51,6 +73,10 @@ struct QuantParams {
 };
 
 int quant_rows_per_group(int K);
+// The one-row-per-workgroup quantizer (16 positions per lane) covers permutation plans with
+// h = 128 and K a multiple of 128 from 1024 to 16384; the general kernel covers the rest.
+bool rpbh_quantize_row_fits(int K, int h, bool gather);
+hipError_t launch_rpbh_quantize_row(QuantParams p, int bits, bool norm_bf16, int cus, hipStream_t stream);
 // gather: apply the permutation through the LDS-staged gather (false only for the identity).
 // Launches a persistent grid of at most two workgroups per compute unit.
 hipError_t launch_rpbh_quantize(QuantParams p, int bits, bool norm_bf16, bool gather, int cus, hipStream_t stream);

@@ -224,7 +224,9 @@ orbit_status quantize_rows(const char* who, orbit_plan p, orbit_codebook cb, con
         q.row_magic = (uint32_t)(((1ull << q.row_shift) + cpr - 1) / cpr);
         q.row_gap = (uint32_t)((ldx - K) * 2);
     }
-    hipError_t e = launch_rpbh_quantize(q, cb->bits, norm_bf16, !p->identity, info.cus, (hipStream_t)stream);
+    hipError_t e = rpbh_quantize_row_fits((int)K, p->h, !p->identity)
+                       ? launch_rpbh_quantize_row(q, cb->bits, norm_bf16, info.cus, (hipStream_t)stream)
+                       : launch_rpbh_quantize(q, cb->bits, norm_bf16, !p->identity, info.cus, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, who);
     return ORBIT_OK;
 }
