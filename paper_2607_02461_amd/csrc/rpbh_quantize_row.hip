@@ -281,20 +281,29 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
     // (T threads), straight from HBM into LDS (global_load_lds_dwordx4: lane i of the wave writes
     // the LDS base + 16 i); the loads complete before the iteration's barrier
     const int G = gridDim.x;
-    const int64_t M = p.M;
+    const int M = (int)p.M;   // below 2^31 (checked by the caller)
     const int nchunks = p.K / 8, wave = tid >> 6, waves = blockDim.x >> 6;
-    auto load_row = [&](int64_t row, int buf) {
+    // A row is K/512 blocks of 64 chunks and a workgroup has at least K/1024 waves, so each wave
+    // brings at most two blocks: `wave` and `wave + waves`.  The row's address is uniform, the lane's
+    // part of a block is 16 * lane bytes further.
+    const int nblk = (nchunks + 63) / 64;
+    const uint32_t lane_off = 16u * (uint32_t)(tid & 63);
+    const bool lane_in_last = (nchunks & 63) == 0 || (tid & 63) < (nchunks & 63);
+    auto load_row = [&](int row, int buf) {
         if (row >= M) return;
-        const char* base = (const char*)p.X + row * p.ldx * 2;
-        for (int blk64 = wave; blk64 * 64 < nchunks; blk64 += waves) {
-            const int c = blk64 * 64 + (tid & 63);
+        const char* base = (const char*)p.X + (int64_t)row * p.ldx * 2;
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+            const int b = wave + v * waves;
+            if (b >= nblk) break;
             __attribute__((address_space(3))) void* dst = (__attribute__((address_space(3))) void*)(
-                (__attribute__((address_space(3))) unsigned char*)smem + p.row_off + 2048u * blk64 + kBufGap * buf);
-            if (c < nchunks) __builtin_amdgcn_global_load_lds((const void*)(base + 16 * c), dst, 16, 0, 0);
+                (__attribute__((address_space(3))) unsigned char*)smem + p.row_off + 2048u * b + kBufGap * buf);
+            if (b < nblk - 1 || lane_in_last)
+                __builtin_amdgcn_global_load_lds((const void*)(base + 1024 * b + lane_off), dst, 16, 0, 0);
         }
     };
 
-    int64_t g = blockIdx.x;
+    int g = blockIdx.x;
     if (g < M) load_row(g, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -313,13 +322,18 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
         // row g + G into the other buffer, whose last reader was row g - G, before the previous
         // barrier
         load_row(g + G, BUF ^ 1);
-        // gather: pair i = positions 2i (low half), 2i+1 (high half)
+        // gather: pair i = positions 2i (low half), 2i+1 (high half).  All sixteen reads are issued
+        // before the first is used (one LDS round trip per row, not two).
+        uint16_t gv[kLaneVals];
+#pragma unroll
+        for (int r = 0; r < kLaneVals; ++r) gv[r] = *(const uint16_t*)(smem + addr[r] + kBufGap * BUF);
+        __builtin_amdgcn_sched_barrier(0);
         uint32_t P[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             u16x2 v;
-            v.x = *(const uint16_t*)(smem + addr[2 * i] + kBufGap * BUF);
-            v.y = *(const uint16_t*)(smem + addr[2 * i + 1] + kBufGap * BUF);
+            v.x = gv[2 * i];
+            v.y = gv[2 * i + 1];
             P[i] = __builtin_bit_cast(uint32_t, v);
         }
 
@@ -350,8 +364,8 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the next row's staging loads
         __syncthreads();
         // row total: every wave sums the block partials in the same fixed order
-        float acc = 0.f;
-        for (int i = lane; i < nb; i += 64) acc += pt[i];
+        float acc = lane < nb ? pt[lane] : 0.f;   // nb <= 128 block partials
+        if (lane + 64 < nb) acc += pt[lane + 64];
         acc += dpp_mov<0xB1>(acc);
         acc += dpp_mov<0x4E>(acc);
         acc += dpp_mov<0x141>(acc);
@@ -381,7 +395,7 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
         }
         uint32_t w[3];
         pack16<BITS>(y, w);
-        if (active) store16<BITS>(p.codes + g * code_row + (int64_t)(blk * 8 + mpos) * (2 * BITS), w);
+        if (active) store16<BITS>(p.codes + (int64_t)g * code_row + (int64_t)(blk * 8 + mpos) * (2 * BITS), w);
         (void)tmp_a;
     };
     for (;;) {
