@@ -240,7 +240,7 @@ def main():
     }
     # The quantizer's launches timed alone as well (back to back, each bracketed by its own events);
     # inside the step each one follows a GEMM, whose power draw holds the clock down for a while.
-    # Rows of K = 512 .. 16384 (a multiple of 128) with h = 128 run the one-row-per-workgroup kernel.
+    # Rows of K = 1024 .. 16384 (a multiple of 128) with h = 128 run the one-row-per-workgroup kernel.
     q_alone = []
     for L in layers:
         fn = (lambda L=L: oq.rpbh_quantize_act(L["plan"], L["cba"], L["X"], 1e-10, L["xc"], L["xn"]))

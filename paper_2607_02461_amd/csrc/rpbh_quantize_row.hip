@@ -1,6 +1,6 @@
 // Fused RPBH rotate -> normalize -> Lloyd-Max encode -> pack for the common case of the
-// activation quantizer and the offline weight pass: a permutation plan with 128-point Hadamard
-// blocks and rows of K = 1024 .. 16384 inputs (a multiple of 128), on gfx950.
+// activation quantizer and the offline weight pass: a permutation plan with Hadamard blocks of
+// h = 128 .. 1024 and rows of K = 1024 .. 16384 inputs (a multiple of 128 and of h), on gfx950.
 //
 // One workgroup holds one row at a time and walks rows persistently (row w, w + G, ...).  Every
 // lane transforms 16 post-permutation positions, so a 128-block belongs to eight consecutive lanes
@@ -229,7 +229,7 @@ __device__ __forceinline__ void store16(uint8_t* dst, const uint32_t (&w)[3]) {
     }
 }
 
-template <int BITS, bool NORM_BF16>
+template <int BITS, bool NORM_BF16, int OUTER>
 __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) {
     extern __shared__ __align__(16) unsigned char smem[];
     const int tid = threadIdx.x;
@@ -240,16 +240,29 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
     float* const part = (float*)(smem + p.part_off);
     unsigned char* const stage = smem + p.row_off;
 
-    // Stages across the block's eight lanes pair lane j with j ^ v for v = 1, 2 (quad_perm) and
-    // 7 (row_half_mirror).  Butterflies along the basis {1, 2, 7} with lower / upper roles from the
-    // dual basis {5, 6, 4} (parity of s_k & v_m is 1 iff k = m) compute the Sylvester transform with
-    // permuted outputs: lane j ends with the 16 outputs of lane position M(j), the XOR of the s_k
-    // whose parity with j is odd.  Each stage leaves the upper partner's value negated; sigma
-    // collects those signs and goes into the encoder scale.
+    // Stages across lanes.  An h-block (h = 128 * 2^OUTER) spans L = h/16 consecutive, aligned lanes
+    // and its Hadamard stages pair lane j with j ^ v along a basis of the lane-index bits:
+    //   h = 128:   v = 1, 2 (quad_perm), 7 (row_half_mirror)                          dual {5, 6, 4}
+    //   h >= 256:  v = 1, 2, 7, 15 (row_mirror), then 16 (ds_swizzle) and 32 (ds_bpermute) as far
+    //              as the block spans                                                  dual {5, 6, 12, 8, 16, 32}
+    // Butterflies along a basis v_k whose lower / upper roles follow the dual basis s_k (parity of
+    // s_k & v_m is 1 iff k = m) compute the Sylvester transform with permuted outputs: lane j ends
+    // with the 16 outputs of lane position M(j), the XOR of the s_k whose parity with j is odd, so
+    // it stores its codes there.  Each stage leaves the upper partner's value negated; sigma, the
+    // parity of j & (XOR of the s_k), collects those signs and goes into the encoder scale.
     auto odd = [](int v) { return (__popc(v) & 1) != 0; };
-    const float sg1 = odd(q & 5) ? -1.f : 1.f, sg2 = odd(q & 6) ? -1.f : 1.f, sg3 = odd(q & 4) ? -1.f : 1.f;
-    const int mpos = (odd(q & 5) ? 5 : 0) ^ (odd(q & 6) ? 6 : 0) ^ (odd(q & 4) ? 4 : 0);
-    const float sigma = odd(q & 7) ? -1.f : 1.f;
+    constexpr int LB = 8 << OUTER;                         // lanes per h-block
+    const int j = tid & (LB - 1);
+    constexpr int d1 = 5, d2 = 6, d3 = OUTER == 0 ? 4 : 12, d4 = 8;
+    const float sg1 = odd(j & d1) ? -1.f : 1.f, sg2 = odd(j & d2) ? -1.f : 1.f, sg3 = odd(j & d3) ? -1.f : 1.f;
+    const float sg4 = odd(j & d4) ? -1.f : 1.f, sg5 = (j & 16) ? -1.f : 1.f, sg6 = (j & 32) ? -1.f : 1.f;
+    int mj = (odd(j & d1) ? d1 : 0) ^ (odd(j & d2) ? d2 : 0) ^ (odd(j & d3) ? d3 : 0);
+    if (OUTER >= 1 && odd(j & d4)) mj ^= d4;
+    mj |= j & ~15;                                         // bits 4, 5: the standard basis
+    constexpr int SX = OUTER == 0 ? 5 ^ 6 ^ 4 : (5 ^ 6 ^ 12 ^ 8) | (OUTER >= 2 ? 16 : 0) | (OUTER >= 3 ? 32 : 0);
+    const float sigma = odd(j & SX) ? -1.f : 1.f;
+    const int mpos = (tid & ~(LB - 1)) + mj;               // output position, in 16-code units
+    const int lane = tid & 63;
 
     // encoder table -> LDS
     for (int i = tid; i < p.ncell; i += blockDim.x) ((float*)smem)[i] = p.enc[i];
@@ -313,7 +326,6 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
     // address is 4 * bits(f) + (table - 4 * 0x4B000000) (mod 2^32): one shift-add
     const uint32_t tab = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem - 0x2C000000u;
     const int64_t code_row = (int64_t)p.K * BITS / 8;
-    const int lane = tid & 63;
 
     // One row from staging buffer BUF (a compile-time constant, so the buffer offset is the LDS
     // instructions' immediate): the loop below alternates the two.
@@ -353,6 +365,28 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
         ORBIT_ROW_DPP16(z, sg1, "quad_perm:[1,0,3,2]");
         ORBIT_ROW_DPP16(z, sg2, "quad_perm:[2,3,0,1]");
         ORBIT_ROW_DPP16(z, sg3, "row_half_mirror");
+        if constexpr (OUTER >= 1) ORBIT_ROW_DPP16(z, sg4, "row_mirror");
+        // lanes 16 apart inside 32 (swizzle, bit mode: xor 16), then 32 apart (bpermute), eight
+        // registers at a time so that the exchanges in flight need few temporaries
+        if constexpr (OUTER >= 2) {
+#pragma unroll
+            for (int c = 0; c < kLaneVals; c += 8) {
+#pragma unroll
+                for (int r = c; r < c + 8; ++r)
+                    z[r] = fmaf(__int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(z[r]), 0x401F)), sg5, z[r]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        if constexpr (OUTER >= 3) {
+#pragma unroll
+            for (int c = 0; c < kLaneVals; c += 8) {
+#pragma unroll
+                for (int r = c; r < c + 8; ++r)
+                    z[r] = fmaf(__int_as_float(__builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __float_as_int(z[r]))), sg6,
+                                z[r]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
 
         // block sums of squares: the eight lanes of a block, in a fixed order
         float ss = (n[0] + n[1]) + (n[2] + n[3]);
@@ -395,7 +429,7 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
         }
         uint32_t w[3];
         pack16<BITS>(y, w);
-        if (active) store16<BITS>(p.codes + (int64_t)g * code_row + (int64_t)(blk * 8 + mpos) * (2 * BITS), w);
+        if (active) store16<BITS>(p.codes + (int64_t)g * code_row + (int64_t)mpos * (2 * BITS), w);
         (void)tmp_a;
     };
     for (;;) {
@@ -408,16 +442,16 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
     }
 }
 
-template <int BITS, bool NB>
+template <int BITS, bool NB, int OUTER>
 hipError_t set_row_smem_limit() {
     static std::atomic<uint64_t> done{0};
-    return raise_lds_limit((const void*)rpbh_quantize_row_kernel<BITS, NB>, 160 * 1024, done);
+    return raise_lds_limit((const void*)rpbh_quantize_row_kernel<BITS, NB, OUTER>, 160 * 1024, done);
 }
 
 }  // namespace
 
 bool rpbh_quantize_row_fits(int K, int h, bool gather) {
-    return gather && h == 128 && K % 128 == 0 && K >= 1024 && K <= 16384;
+    return gather && h >= 128 && h <= 1024 && K % 128 == 0 && K % h == 0 && K >= 1024 && K <= 16384;
 }
 
 hipError_t launch_rpbh_quantize_row(QuantParams p, int bits, bool norm_bf16, int cus, hipStream_t stream) {
@@ -430,24 +464,32 @@ hipError_t launch_rpbh_quantize_row(QuantParams p, int bits, bool norm_bf16, int
     if (smem > 160u * 1024u) return hipErrorInvalidValue;
     // persistent: exactly as many workgroups as are resident at once (a grid larger than that would
     // start its last workgroups only when earlier ones had finished all their rows)
-#define ORBIT_ROW_LAUNCH(B, NB)                                                                     \
+#define ORBIT_ROW_LAUNCH(B, NB, OU)                                                                 \
     do {                                                                                            \
-        const hipError_t e = set_row_smem_limit<B, NB>();                                           \
+        const hipError_t e = set_row_smem_limit<B, NB, OU>();                                       \
         if (e != hipSuccess) return e;                                                              \
-        const int64_t want = (int64_t)cus * resident_blocks((const void*)rpbh_quantize_row_kernel<B, NB>, threads, smem); \
+        const int64_t want = (int64_t)cus * resident_blocks((const void*)rpbh_quantize_row_kernel<B, NB, OU>, threads, smem); \
         const int grid = (int)(p.M < want ? p.M : want);                                            \
-        hipLaunchKernelGGL((rpbh_quantize_row_kernel<B, NB>), dim3(grid), dim3(threads), smem, stream, p); \
+        hipLaunchKernelGGL((rpbh_quantize_row_kernel<B, NB, OU>), dim3(grid), dim3(threads), smem, stream, p); \
+    } while (0)
+#define ORBIT_ROW_OUTER(B, NB)                                                                      \
+    do {                                                                                            \
+        if (p.outer == 0) ORBIT_ROW_LAUNCH(B, NB, 0);                                               \
+        else if (p.outer == 1) ORBIT_ROW_LAUNCH(B, NB, 1);                                          \
+        else if (p.outer == 2) ORBIT_ROW_LAUNCH(B, NB, 2);                                          \
+        else ORBIT_ROW_LAUNCH(B, NB, 3);                                                            \
     } while (0)
 #define ORBIT_ROW_BITS(NB)                                                                          \
     do {                                                                                            \
-        if (bits == 2) ORBIT_ROW_LAUNCH(2, NB);                                                     \
-        else if (bits == 3) ORBIT_ROW_LAUNCH(3, NB);                                                \
-        else if (bits == 6) ORBIT_ROW_LAUNCH(6, NB);                                                \
-        else ORBIT_ROW_LAUNCH(4, NB);                                                               \
+        if (bits == 2) ORBIT_ROW_OUTER(2, NB);                                                      \
+        else if (bits == 3) ORBIT_ROW_OUTER(3, NB);                                                 \
+        else if (bits == 6) ORBIT_ROW_OUTER(6, NB);                                                 \
+        else ORBIT_ROW_OUTER(4, NB);                                                                \
     } while (0)
     if (norm_bf16) ORBIT_ROW_BITS(true);
     else ORBIT_ROW_BITS(false);
 #undef ORBIT_ROW_BITS
+#undef ORBIT_ROW_OUTER
 #undef ORBIT_ROW_LAUNCH
     return hipGetLastError();
 }
