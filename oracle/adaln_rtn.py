@@ -11,9 +11,11 @@ Readings taken where the paper is silent (it does not spell out the rounding gri
   * symmetric scaling per group of 64 consecutive inputs of a weight row;
   * the group's scale is the FP16 rounding (to nearest even, saturating at the largest finite
     FP16) of the FP32 quotient absmax / 7, and a group whose scale rounds to 0 has codes 0;
-  * q = clamp(RNE(w / scale), -8, 7), the quotient formed in FP32 with the FP16 scale: the same
-    two IEEE roundings the kernel performs, so scales and codes are defined bit for bit
-    (|w / scale| <= 7 up to the scale's rounding, so the clamp only guards);
+  * q = clamp(RNE(w / scale), -8, 7), the quotient formed in FP32 with the stored FP16 scale
+    (the scale a dequantizer reads back, so q is the nearest integer multiple of the scale that
+    is actually stored; FP32 holds every BF16 weight exactly and the quotient needs only one
+    IEEE rounding before the integer rounding, so the definition is exact bit for bit;
+    |w / scale| <= 7 up to the scale's rounding, so the clamp only guards);
   * storage: q + 8 (offset binary, 0..15) as LSB-first nibbles, element 2j in the low nibble
     of byte j; scales as FP16 [N][K/64].
 The dequantized weight is q * scale and the layer is Y = X W_deq^T (+ bias) with BF16 X, here
