@@ -66,7 +66,7 @@ def source_digest():
     """Digest of the kernel sources; traffic counters taken from other sources are not used."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("rpbh_quantize.hip", "lut_gemm.hip"):
+    for f in ("rpbh_quantize.hip", "rpbh_quantize_row.hip", "lut_gemm.hip"):
         with open(os.path.join(ROOT, "paper_2607_02461_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -240,14 +240,16 @@ def main():
     }
     # The quantizer's launches timed alone as well (back to back, each bracketed by its own events);
     # inside the step each one follows a GEMM, whose power draw holds the clock down for a while.
-    # Rows of K = 1024 .. 16384 (a multiple of 128) with h = 128 run the one-row-per-workgroup kernel.
+    # Rows of K = 1024 .. 16384 (a multiple of 128 and of h) with h = 128 .. 1024 run the
+    # one-row-per-workgroup kernel; its last template argument is log2(h / 128).
     q_alone = []
     for L in layers:
         fn = (lambda L=L: oq.rpbh_quantize_act(L["plan"], L["cba"], L["X"], 1e-10, L["xc"], L["xn"]))
         q_alone.append(_timed(fn, args.part_reps)[0])
-    qkern = [(f"rpbh_quantize_row_kernel<{L['lin'].ba},false>" if L["lin"].h == 128 and L["lin"].K % 128 == 0
+    qkern = [(f"rpbh_quantize_row_kernel<{L['lin'].ba}, false, {L['lin'].h.bit_length() - 8}>"
+              if 128 <= L["lin"].h <= 1024 and L["lin"].K % 128 == 0 and L["lin"].K % L["lin"].h == 0
               and 1024 <= L["lin"].K <= 16384 else
-              f"rpbh_quantize_kernel<{L['lin'].ba},false,{'true' if L['lin'].h > 128 else 'false'},true>")
+              f"rpbh_quantize_kernel<{L['lin'].ba}, false, {'true' if L['lin'].h > 128 else 'false'}, true>")
              for L in layers]
     qa_gbs = float(qbytes.sum()) / (sum(q_alone) * 1e-3) / 1e9
     roofline_q = {
