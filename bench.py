@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "orbit_qlinear TFLOP/s + rpbh_quantize_act GB/s (% of MI355X roofline)"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
-FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak
+MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak (the same for fp16)
 
 
 def parse():
@@ -227,9 +227,9 @@ def main():
         "kernel": dom[0]["kernel"],
         "bound": "mfma",
         "achieved": dom_flops / (dom_ms * 1e-3) / 1e12,
-        "peak": FP16_MFMA_PEAK_TFLOPS,
+        "peak": MFMA_PEAK_TFLOPS,
         "unit": "TFLOP/s",
-        "frac": dom_flops / (dom_ms * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS,
+        "frac": dom_flops / (dom_ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS,
         "traffic": (traffic or {}).get("gemm_bytes_per_launch"),
         "achieved_is": "2*rows*N*K of each launch of this kernel in the step / its HIP-event launch time, "
                        "over the launches listed in 'launches'",
@@ -308,7 +308,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16",
+        "dtype": "bf16",
         "data": "synthetic",
         "config": {
             "workload": wl.name,
@@ -316,13 +316,13 @@ def main():
             "linears": [{"name": L["lin"].name, "M": L["lin"].M, "K": L["lin"].K, "N": L["lin"].N,
                          "bits": f"W{L['lin'].bw}A{L['lin'].ba}", "h": L["lin"].h} for L in layers],
             "value_is": "GEMM flops of the step / step time (quantizer + GEMM per linear)",
-            "arith": "quantizer fp32; GEMM fp16 MFMA operands, fp32 accumulate",
+            "arith": "quantizer fp32; GEMM bf16 MFMA operands (levels dequantized to bf16), fp32 accumulate",
             # inputs above the 256 MB Infinity Cache stream from HBM on every step
             "cache": "cold" if min(L["X"].numel() * 2 for L in layers) > (256 << 20) else "warm",
         },
         "components": {
             "orbit_qlinear_tflops": gemm_tflops,
-            "orbit_qlinear_frac_of_fp16_peak": gemm_tflops / FP16_MFMA_PEAK_TFLOPS,
+            "orbit_qlinear_frac_of_bf16_peak": gemm_tflops / MFMA_PEAK_TFLOPS,
             "rpbh_quantize_act_gbs": quant_gbs,
             "rpbh_quantize_act_frac_of_hbm": quant_gbs / HBM_PEAK_GBS,
             "quant_ms": [float(v) for v in quant_ms],
@@ -569,7 +569,7 @@ def gemm_parts(oq, L, reps):
                 + ("+lut_gemm_reduce" if splits > 1 else ""))
         out.append({"linear": lin.name, "kernel": name, "rows": [r0, r1], "N": N, "K": K, "splits": 1 if big else splits,
                     "flops": fl, "ms": mean, "ms_median": med, "ms_min": mn,
-                    "tflops": fl / (mean * 1e-3) / 1e12, "frac": fl / (mean * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS})
+                    "tflops": fl / (mean * 1e-3) / 1e12, "frac": fl / (mean * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS})
     return out
 
 
@@ -623,7 +623,7 @@ def configs_sweep(oq, workloads, dev, reps):
                     "quant_ms": q[0], "quant_ms_min": q[2], "quant_gbs": qb / (q[0] * 1e-3) / 1e9,
                     "quant_frac_of_hbm": qb / (q[0] * 1e-3) / 1e9 / HBM_PEAK_GBS,
                     "gemm_ms": g[0], "gemm_ms_min": g[2], "gemm_tflops": fl / (g[0] * 1e-3) / 1e12,
-                    "gemm_frac_of_fp16_peak": fl / (g[0] * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS})
+                    "gemm_frac_of_bf16_peak": fl / (g[0] * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS})
         del wc, wn, xc, xn, Y, ws
     del flush
     return {"cache": "cold: operands below 256 MB evicted before every timed launch", "linears": res}
@@ -754,7 +754,7 @@ def trunk_sweep(oq, workloads, dev, steps, warmup=1):
     return {"workload": wl.name, "blocks": wl.repeat, "linears_per_step": n, "M": M, "steps": steps,
             "step_ms": step_ms, "step_tflops": flops / (step_ms * 1e-3) / 1e12,
             "gemm_ms_sum": g_ms, "gemm_tflops": flops / (g_ms * 1e-3) / 1e12,
-            "gemm_frac_of_fp16_peak": flops / (g_ms * 1e-3) / 1e12 / FP16_MFMA_PEAK_TFLOPS,
+            "gemm_frac_of_bf16_peak": flops / (g_ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS,
             "quant_ms_sum": q_ms, "quant_gbs": qbytes / (q_ms * 1e-3) / 1e9,
             "quant_frac_of_hbm": qbytes / (q_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "weight_pass_ms": wp_ms, "weight_pass_gbs": wp_bytes / (wp_ms * 1e-3) / 1e9,
@@ -903,7 +903,7 @@ def parity_vs_oracle(oracle, layers, prepared, last, gemm_rows=256, band=1e-5):
     near-ties (|u - tau| > 1e-5); within a near-tie only the two codes across the nearest threshold are
     nearest centroids (Eq. (3) ties there), so other codes count as invalid.  Norms to 1e-5 (s) and
     one bf16 ulp (r').  The layer on gemm_rows rows against the fp64 contraction of the GPU's own codes,
-    norms and fp16 levels: relative Frobenius error and the worst element over the per-element bar
+    norms and bf16 levels: relative Frobenius error and the worst element over the per-element bar
     1e-4 s_n r'_i ||a_n|| ||b_i||."""
     res = []
     for L, (lin, plan, cba, cbw, cw, r, X), (cx, s, Ux) in zip(layers, prepared, last):
@@ -926,7 +926,7 @@ def parity_vs_oracle(oracle, layers, prepared, last, gemm_rows=256, band=1e-5):
         entry["s_max_rel_err"] = float(np.max(np.abs(gs - s) / np.maximum(s, 1e-30)))
         entry["r_max_err_bf16_ulps"] = float(np.max(np.abs(gr - r) / ulp))
         m = min(gemm_rows, n)
-        la, lw = oracle.fp16_round(cba.levels), oracle.fp16_round(cbw.levels)
+        la, lw = oracle.bf16_round(cba.levels), oracle.bf16_round(cbw.levels)
         ref = oracle.qlinear(gx[:m], gs[:m], la, gw, gr, lw)
         Y = L["Y"][:m].double().cpu().numpy()
         unit = (gs[:m] * np.linalg.norm(la[gx[:m]], axis=1))[:, None] * (gr * np.linalg.norm(lw[gw], axis=1))[None, :]

@@ -130,12 +130,14 @@ void rpbh_plan_destroy(orbit_plan p);
 orbit_status lloydmax_codebook(int32_t bits, int64_t d, orbit_codebook* out);
 
 /*
- * Read back a codebook: levels (2^b, ascending), thresholds (2^b - 1), and the fp16 image
- * of the levels that the GEMM decodes to (2^b IEEE half bit patterns, round-to-nearest-even
- * of the fp64 levels).  Any output pointer may be NULL.
+ * Read back a codebook: levels (2^b, ascending), thresholds (2^b - 1), and the bf16 image of
+ * the levels that the GEMM decodes to (2^b bfloat16 bit patterns, the fp64 levels rounded once
+ * to nearest, ties to even).  The paper dequantizes codes to BF16 and multiplies in BF16 (its
+ * efficiency measurements and limitations section); the GEMM does the same with fp32
+ * accumulation.  Any output pointer may be NULL.
  */
 orbit_status lloydmax_codebook_get(orbit_codebook c, int32_t* bits, int64_t* d, double* levels,
-                                   double* thresholds, uint16_t* lut_f16);
+                                   double* thresholds, uint16_t* lut_bf16);
 
 /*
  * lloydmax_codebook_upload -- copy the codebook's encoder table (the quantizer's nearest-level
@@ -203,8 +205,9 @@ orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t
  * orbit_qlinear -- the quantized layer on codes (Sec. 4.3: W'x' = W Pi^T Pi x = W x; the
  * codebook GEMM named as future work in the paper's limitations):
  *     Y[n][i] = x_norm[n] * w_norm[i] * sum_k L_a[x_code[n][k]] * L_w[w_code[i][k]],
- * where L_a, L_w are the fp16 images of the two codebooks' levels.  Products are exact in
- * fp32 and accumulate in fp32 on the matrix cores.
+ * where L_a, L_w are the bf16 images of the two codebooks' levels (codes dequantized to BF16
+ * and multiplied in BF16, as the paper computes its layers).  Products are exact in fp32 and
+ * accumulate in fp32 on the matrix cores.
  *
  *   cb_a, x_codes, x_norm   activation codebook (bits b_a) and the outputs of
  *                           rpbh_quantize_act for M rows
@@ -216,7 +219,7 @@ orbit_status rpbh_quantize_act(orbit_plan p, orbit_codebook cb_a, const uint16_t
  * Pointers: codes 16-byte aligned, x_norm 4-byte, w_norm 2-byte, Y 4-byte aligned (Y 16-byte
  * aligned with ldy % 4 == 0 and w_norm 8-byte aligned enable vector stores; other layouts are
  * handled element-wise).  The 4-bit decoder relies on the codebook's exact antisymmetry in
- * fp16 (L[15-c] = -L[c]), which lloydmax_codebook guarantees; ORBIT_EINTERNAL otherwise.
+ * bf16 (L[15-c] = -L[c]), which lloydmax_codebook guarantees; ORBIT_EINTERNAL otherwise.
  * Errors: ORBIT_EINVAL (null pointer, dimension mismatch, ldy < N); ORBIT_EUNSUPPORTED
  * (activation bits not in {2, 3, 4, 6}, weight bits outside 2..4, K not a multiple of 64,
  * M or N above 2^31 - 1 or more than 2^27 output tiles of 256 x 256); ORBIT_EHIP.  M = 0 or

@@ -157,10 +157,10 @@ class Codebook:
         n = 1 << self.bits
         self.levels = np.empty(n, dtype=np.float64)
         self.thresholds = np.empty(n - 1, dtype=np.float64)
-        self.lut_f16 = np.empty(n, dtype=np.uint16)
+        self.lut_bf16 = np.empty(n, dtype=np.uint16)
         _check("lloydmax_codebook_get", lib().lloydmax_codebook_get(handle, None, None, self.levels.ctypes.data,
                                                                      self.thresholds.ctypes.data,
-                                                                     self.lut_f16.ctypes.data))
+                                                                     self.lut_bf16.ctypes.data))
 
     @property
     def handle(self):

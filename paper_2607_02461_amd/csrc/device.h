@@ -94,8 +94,8 @@ struct GemmParams {
     const uint16_t* bias;  // bf16 [N] or null, added after the rescaling
     int gelu;              // apply x * Phi(x) (erfc to 1.2e-7 fractional error) after the bias
     int out_bf16;          // store Y as bf16 (round to nearest even) instead of fp32
-    uint16_t lut_a[64];    // fp16 levels (2^ba used)
-    uint16_t lut_w[16];    // fp16 levels (2^bw used)
+    uint16_t lut_a[64];    // bf16 levels (2^ba used)
+    uint16_t lut_w[16];    // bf16 levels (2^bw used)
     // K-split of the 128x128 kernel's rows (caller workspace): fp32 partial sums [splits][M][N]
     // of the rows it runs, each split split_steps K-steps of 64; ws = null runs unsplit
     float* ws;

@@ -368,11 +368,11 @@ orbit_status orbit_qlinear_ws(orbit_codebook cb_a, const uint8_t* x_codes, const
         // the 4-bit decoder reads the positive half and mirrors it
         if (cb->bits != 4) continue;
         for (int c = 0; c < 8; ++c)
-            if (cb->lut_f16[15 - c] != (uint16_t)(cb->lut_f16[c] ^ 0x8000u))
-                return fail(ORBIT_EINTERNAL, "orbit_qlinear: 4-bit fp16 levels are not antisymmetric");
+            if (cb->lut_bf16[15 - c] != (uint16_t)(cb->lut_bf16[c] ^ 0x8000u))
+                return fail(ORBIT_EINTERNAL, "orbit_qlinear: 4-bit bf16 levels are not antisymmetric");
     }
-    for (int j = 0; j < 64; ++j) g.lut_a[j] = j < (1 << cb_a->bits) ? cb_a->lut_f16[j] : 0;
-    for (int j = 0; j < 16; ++j) g.lut_w[j] = j < (1 << cb_w->bits) ? cb_w->lut_f16[j] : 0;
+    for (int j = 0; j < 64; ++j) g.lut_a[j] = j < (1 << cb_a->bits) ? cb_a->lut_bf16[j] : 0;
+    for (int j = 0; j < 16; ++j) g.lut_w[j] = j < (1 << cb_w->bits) ? cb_w->lut_bf16[j] : 0;
     hipError_t e = launch_lut_gemm(g, cb_a->bits, cb_w->bits, info.cus, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "orbit_qlinear");
     return ORBIT_OK;

@@ -254,6 +254,18 @@ bool lloyd_max_positive_half(int64_t d, int bits, std::vector<double>& p_out) {
     return true;
 }
 
+// BF16 bit pattern of an fp64 value, rounded once to 8 significant bits, ties to even (no double
+// rounding through fp32).  Levels are finite and far inside the bf16 range.
+uint16_t bf16_bits_rne(double v) {
+    if (v == 0.0) return std::signbit(v) ? 0x8000u : 0u;
+    int e;
+    const double m = std::frexp(v, &e);                       // v = m 2^e, 0.5 <= |m| < 1
+    const float r = (float)std::ldexp(std::nearbyint(std::ldexp(m, 8)), e - 8);  // exact in fp32
+    uint32_t u;
+    std::memcpy(&u, &r, 4);
+    return (uint16_t)(u >> 16);
+}
+
 }  // namespace
 
 void build_enc_table(orbit_codebook_s* c) {
@@ -397,13 +409,8 @@ orbit_status lloydmax_codebook(int32_t bits, int64_t d, orbit_codebook* out) {
     c->thresholds.resize(n - 1);
     for (int j = 0; j + 1 < n; ++j) c->thresholds[j] = 0.5 * (c->levels[j] + c->levels[j + 1]);
     build_enc_table(c);
-    c->lut_f16.resize(n);
-    for (int j = 0; j < n; ++j) {
-        _Float16 hv = (_Float16)c->levels[j];
-        uint16_t bitsv;
-        std::memcpy(&bitsv, &hv, 2);
-        c->lut_f16[j] = bitsv;
-    }
+    c->lut_bf16.resize(n);
+    for (int j = 0; j < n; ++j) c->lut_bf16[j] = bf16_bits_rne(c->levels[j]);
     const orbit_status st = upload_on_create(nullptr, c);
     if (st != ORBIT_OK) {
         lloydmax_codebook_destroy(c);
@@ -414,7 +421,7 @@ orbit_status lloydmax_codebook(int32_t bits, int64_t d, orbit_codebook* out) {
 }
 
 orbit_status lloydmax_codebook_get(orbit_codebook c, int32_t* bits, int64_t* d, double* levels, double* thresholds,
-                                   uint16_t* lut_f16) {
+                                   uint16_t* lut_bf16) {
     clear_error();
     if (!c) return fail(ORBIT_EINVAL, "lloydmax_codebook_get: codebook is NULL");
     if (bits) *bits = c->bits;
@@ -422,7 +429,7 @@ orbit_status lloydmax_codebook_get(orbit_codebook c, int32_t* bits, int64_t* d, 
     const size_t n = c->levels.size();
     if (levels) std::memcpy(levels, c->levels.data(), n * sizeof(double));
     if (thresholds) std::memcpy(thresholds, c->thresholds.data(), (n - 1) * sizeof(double));
-    if (lut_f16) std::memcpy(lut_f16, c->lut_f16.data(), n * sizeof(uint16_t));
+    if (lut_bf16) std::memcpy(lut_bf16, c->lut_bf16.data(), n * sizeof(uint16_t));
     return ORBIT_OK;
 }
 

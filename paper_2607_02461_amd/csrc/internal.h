@@ -47,13 +47,13 @@ struct EncTable {
     std::vector<float> bias;
 };
 
-// C^(d,b): ascending levels, midpoint thresholds, fp16 image of the levels.
+// C^(d,b): ascending levels, midpoint thresholds, bf16 image of the levels (the GEMM's operands).
 struct orbit_codebook_s {
     int32_t bits = 0;
     int64_t d = 0;
     std::vector<double> levels;
     std::vector<double> thresholds;
-    std::vector<uint16_t> lut_f16;
+    std::vector<uint16_t> lut_bf16;
     EncTable enc;
     std::mutex mu;
     float* dev_enc[orbit::kMaxDevices] = {};

@@ -1,14 +1,18 @@
-// LUT-decode GEMM on packed Lloyd-Max codes for gfx950 (fp16 MFMA, fp32 accumulate).
+// LUT-decode GEMM on packed Lloyd-Max codes for gfx950 (bf16 MFMA, fp32 accumulate).
 //
 // Computes Y[n][i] = s_n * r'_i * sum_k L_a[xc[n][k]] * L_w[wc[i][k]]: the rotation cancels in
 // the product (Sec. 4.3), so the two code sets are contracted directly in the rotated basis;
 // the paper's limitations section names this codebook GEMM as the missing kernel.
 //
+// Operands: codes are dequantized to the bf16 images of the levels and multiplied in bf16, the
+// arithmetic the paper runs its layers in (codes dequantized to BF16, matmul in BF16); on the
+// matrix cores the products accumulate in fp32.
+//
 // Decode: codes are widened to bytes and looked up with v_perm_b32 against byte tables of the
-// fp16 levels (low bytes and high bytes of the 2^b levels, 8 entries per register pair), which
-// needs no memory access.  Each code of a block tile is decoded exactly once, into an fp16 tile
-// in LDS that the matrix cores then read.  fp16 products are exact in fp32, so the result
-// differs from an fp64 evaluation with the same fp16 levels only by fp32 accumulation.
+// bf16 levels (low bytes and high bytes of the 2^b levels, 8 entries per register pair), which
+// needs no memory access.  Each code of a block tile is decoded exactly once, into a bf16 tile
+// in LDS that the matrix cores then read.  bf16 products are exact in fp32, so the result
+// differs from an fp64 evaluation with the same bf16 levels only by fp32 accumulation.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -20,7 +24,7 @@ namespace orbit {
 
 namespace {
 
-typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 128, BN = 128, BK = 64;
@@ -36,7 +40,7 @@ struct ByteTables {
 
 // Tables of at most eight levels hold every level.  The 4-bit table holds the positive half
 // L[8..15] only: the codebook is antisymmetric (L[15-c] = -L[c], Sec. 3's symmetric marginal),
-// so a code below 8 reads the mirrored entry and sets the fp16 sign bit.  The host checks the
+// so a code below 8 reads the mirrored entry and sets the bf16 sign bit.  The host checks the
 // antisymmetry bit for bit before launching.
 template <int BITS>
 __device__ __forceinline__ ByteTables make_tables(const uint16_t* lut) {
@@ -59,17 +63,17 @@ __device__ __forceinline__ ByteTables make_tables(const uint16_t* lut) {
 }
 
 // Canonical slot order.  The eight codes of each aligned group k0..k7 are written to eight
-// consecutive fp16 slots in the order k0 k2 k4 k6 k1 k3 k5 k7.  Both operands use the same order
+// consecutive bf16 slots in the order k0 k2 k4 k6 k1 k3 k5 k7.  Both operands use the same order
 // for every bit width, so every MFMA still contracts matching k; the order is the one the 4-bit
 // decoder produces without any byte shuffling (even and odd nibbles of a code word).
 
-// Four table indices (one per byte of sel, each below 8) -> fp16 low and high bytes.
+// Four table indices (one per byte of sel, each below 8) -> bf16 low and high bytes.
 __device__ __forceinline__ void lookup_bytes(uint32_t sel, const ByteTables& t, uint32_t& lo, uint32_t& hi) {
     lo = __builtin_amdgcn_perm(t.lo[1], t.lo[0], sel);
     hi = __builtin_amdgcn_perm(t.hi[1], t.hi[0], sel);
 }
 
-// low/high byte words of four values -> two fp16x2 words (values 0,1 and 2,3)
+// low/high byte words of four values -> two bf16x2 words (values 0,1 and 2,3)
 __device__ __forceinline__ void interleave(uint32_t lo, uint32_t hi, uint32_t& d0, uint32_t& d1) {
     d0 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);  // [lo0 hi0 lo1 hi1]
     d1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);  // [lo2 hi2 lo3 hi3]
@@ -102,7 +106,7 @@ __device__ __forceinline__ void decode8_small(const Codes<BITS>& w, int g, const
     interleave(lo, hi, out[2], out[3]);
 }
 
-// 6-bit groups: 64 levels are too many for byte permutes, so the fp16 levels sit in a 64-entry
+// 6-bit groups: 64 levels are too many for byte permutes, so the bf16 levels sit in a 64-entry
 // LDS table with a 4-byte stride; every entry has its own bank, so a wave's 64 lookups never
 // conflict (equal codes broadcast).
 __device__ __forceinline__ void decode8_lds6(const Codes<6>& w, int g, const uint32_t* tab, uint32_t (&out)[4]) {
@@ -121,7 +125,7 @@ __device__ __forceinline__ void decode8_lds6(const Codes<6>& w, int g, const uin
     out[3] = v[5] | (v[7] << 16);
 }
 
-// Group g (codes 8g .. 8g+7) of 32 packed codes (4*BITS bytes, LSB-first) -> four fp16x2 words
+// Group g (codes 8g .. 8g+7) of 32 packed codes (4*BITS bytes, LSB-first) -> four bf16x2 words
 // in canonical slot order.
 template <int BITS>
 __device__ __forceinline__ void decode8(const Codes<BITS>& w, int g, const ByteTables& t, const uint32_t* tab6,
@@ -221,9 +225,9 @@ __device__ __forceinline__ void store_one(const GemmParams& p, int64_t row, int6
 // fewer) and stores its raw sums to p.ws[z][M][N]; lut_gemm_reduce applies the epilogue.
 template <int BA, int BW, bool SPLIT>
 __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
-    __shared__ __align__(16) _Float16 As[BM * LDS_STRIDE];
-    __shared__ __align__(16) _Float16 Bs[BN * LDS_STRIDE];
-    __shared__ uint32_t tab6[BA == 6 ? 64 : 1];  // 6-bit activation levels (fp16 in the low half)
+    __shared__ __align__(16) __bf16 As[BM * LDS_STRIDE];
+    __shared__ __align__(16) __bf16 Bs[BN * LDS_STRIDE];
+    __shared__ uint32_t tab6[BA == 6 ? 64 : 1];  // 6-bit activation levels (bf16 in the low half)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
@@ -285,18 +289,18 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
         __syncthreads();
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
-            half8 a[2], b[2];
+            bf16x8 a[2], b[2];
 #pragma unroll
             for (int i = 0; i < 2; ++i)
-                a[i] = *(const half8*)(As + (wm * 64 + i * 32 + (lane & 31)) * LDS_STRIDE + kk * 16 + (lane >> 5) * 8);
+                a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + (lane & 31)) * LDS_STRIDE + kk * 16 + (lane >> 5) * 8);
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                b[j] = *(const half8*)(Bs + (wn * 64 + j * 32 + (lane & 31)) * LDS_STRIDE + kk * 16 + (lane >> 5) * 8);
+                b[j] = *(const bf16x8*)(Bs + (wn * 64 + j * 32 + (lane & 31)) * LDS_STRIDE + kk * 16 + (lane >> 5) * 8);
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[i], b[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
         __syncthreads();
     };
@@ -349,7 +353,7 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
 
 // ------------------------------------------------------------------------------------------
 // Large-problem kernel: 256x256 block tiles, K-step 64, eight waves of 128x64 each.  Every code
-// of a block tile is decoded once per K-step into a double-buffered fp16 tile in LDS (147 KB),
+// of a block tile is decoded once per K-step into a double-buffered bf16 tile in LDS (147 KB),
 // which halves the decodes per flop of the 128x128 kernel.  While the matrix cores work on step
 // s, each wave decodes step s+1 into the other stage, a quarter per 16-wide k slice, and the
 // codes of step s+2 are in flight.  Block tiles are visited so that the
@@ -362,7 +366,7 @@ constexpr int GROUP_M = 8;                            // block rows per L2 group
 
 template <int BA, int BW>
 __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, int ntn, int per_xcd) {
-    extern __shared__ __align__(16) _Float16 lds[];  // [stage][A, B][256][72]
+    extern __shared__ __align__(16) __bf16 lds[];  // [stage][A, B][256][72]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 2, wn = wave & 3;
 
@@ -402,9 +406,9 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
 
     const int nk = p.K / BK2;
     const int64_t astep = BK2 * BA / 8, bstep = BK2 * BW / 8;
-    _Float16* const a_dst0 = lds + lr * LDS2_STRIDE + lh * 32;  // this thread's decode slots, stage 0
-    const _Float16* const a_frag0 = lds + (wm * 128 + (lane & 31)) * LDS2_STRIDE + (lane >> 5) * 8;
-    const _Float16* const b_frag0 = lds + LDS2_TILE + (wn * 64 + (lane & 31)) * LDS2_STRIDE + (lane >> 5) * 8;
+    __bf16* const a_dst0 = lds + lr * LDS2_STRIDE + lh * 32;  // this thread's decode slots, stage 0
+    const __bf16* const a_frag0 = lds + (wm * 128 + (lane & 31)) * LDS2_STRIDE + (lane >> 5) * 8;
+    const __bf16* const b_frag0 = lds + LDS2_TILE + (wn * 64 + (lane & 31)) * LDS2_STRIDE + (lane >> 5) * 8;
     constexpr int STAGE = 2 * LDS2_TILE;
 
     Codes<BA> wa, xa;
@@ -427,12 +431,12 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     __syncthreads();
 
     // fragments of one 16-wide k slice of a stage
-    half8 a[2][4], b[2][2];
-    auto read_frags = [&](int stage, int kk, half8 (&af)[4], half8 (&bf)[2]) {
+    bf16x8 a[2][4], b[2][2];
+    auto read_frags = [&](int stage, int kk, bf16x8 (&af)[4], bf16x8 (&bf)[2]) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) af[i] = *(const half8*)(a_frag0 + stage + i * 32 * LDS2_STRIDE + kk * 16);
+        for (int i = 0; i < 4; ++i) af[i] = *(const bf16x8*)(a_frag0 + stage + i * 32 * LDS2_STRIDE + kk * 16);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) bf[j] = *(const half8*)(b_frag0 + stage + j * 32 * LDS2_STRIDE + kk * 16);
+        for (int j = 0; j < 2; ++j) bf[j] = *(const bf16x8*)(b_frag0 + stage + j * 32 * LDS2_STRIDE + kk * 16);
     };
     auto decode_group = [&](int nxt, int g, const Codes<BA>& ca, const Codes<BW>& cb) {
         uint32_t da[4], db[4];
@@ -476,7 +480,7 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(b[f][j], a[f][i], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[f][j], a[f][i], acc[i][j], 0, 0, 0);
             // issue order inside the slice: next fragments first, then each MFMA followed by a
             // share of the decode, the decoded rows' LDS writes last
             __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
@@ -589,7 +593,7 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
 template <int BA, int BW>
 hipError_t launch_big(const GemmParams& p, hipStream_t stream) {
     static std::atomic<uint64_t> attr{0};
-    const size_t smem = (size_t)2 * 2 * LDS2_TILE * sizeof(_Float16) + (BA == 6 ? 64 * sizeof(uint32_t) : 0);
+    const size_t smem = (size_t)2 * 2 * LDS2_TILE * sizeof(__bf16) + (BA == 6 ? 64 * sizeof(uint32_t) : 0);
     const hipError_t e = raise_lds_limit((const void*)lut_gemm_big<BA, BW>, (int)smem, attr);
     if (e != hipSuccess) return e;
     const int ntm = (int)((p.M + BM2 - 1) / BM2), ntn = (int)((p.N + BN2 - 1) / BN2);

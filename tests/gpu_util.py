@@ -15,7 +15,7 @@ import paper_2607_02461_amd as oq
 TIE_BAND = 1e-5      # |u - tau| at or below this is a near-tie: counted, not a failure
 GEMM_REL_F = 2e-3    # relative Frobenius bar for the GEMM against fp64 with identical codes/levels
 # Per-element bar of the contraction: |Y[n,i] - ref[n,i]| <= ELEM_TOL * s_n r'_i ||a_n|| ||b_i||, with
-# a_n = L_a[x_code[n]] and b_i = L_w[w_code[i]] (fp16 levels).  The fp16 products are exact in fp32;
+# a_n = L_a[x_code[n]] and b_i = L_w[w_code[i]] (bf16 levels).  The bf16 products are exact in fp32;
 # what remains is the fp32 sum of K of them (plus split partials and a few epilogue roundings).  The
 # probabilistic bound on a sum of n terms (Higham and Mary, SIAM J. Sci. Comput. 2019),
 # lambda sqrt(n) u sum|a_k b_k| with u = 2^-24 and lambda = 10, is below 8e-5 ||a|| ||b|| (Cauchy-Schwarz)
@@ -115,10 +115,10 @@ def assert_codes(name, stats):
         f"{name}: {stats['near_tie_invalid']} near-tie codes neither the oracle's nor its neighbour across the threshold"
 
 
-def qlinear_oracle_fp16(xc, xs, cba_bits, wc, wr, cbw_bits, K):
-    """The oracle contraction with the fp16 images of the oracle's own codebooks."""
-    la = oracle.fp16_round(oracle.lloydmax_codebook(cba_bits, K).levels)
-    lw = oracle.fp16_round(oracle.lloydmax_codebook(cbw_bits, K).levels)
+def qlinear_oracle_bf16(xc, xs, cba_bits, wc, wr, cbw_bits, K):
+    """The oracle contraction with the bf16 images of the oracle's own codebooks."""
+    la = oracle.bf16_round(oracle.lloydmax_codebook(cba_bits, K).levels)
+    lw = oracle.bf16_round(oracle.lloydmax_codebook(cbw_bits, K).levels)
     return oracle.qlinear(xc, xs, la, wc, wr, lw)
 
 

@@ -59,7 +59,7 @@ def pipeline_check(name, X, W, bw, ba, seed, rows=128, cols=256, plan_seed=0):
     r_ulps = float(np.max(np.abs(gr - r) / np.ldexp(1.0, np.frexp(np.maximum(r, 1e-30))[1] - 8)))
     assert s_err <= 1e-5 and r_ulps <= 1.0
 
-    la, lw = oracle.fp16_round(oca.levels), oracle.fp16_round(ocw.levels)
+    la, lw = oracle.bf16_round(oca.levels), oracle.bf16_round(ocw.levels)
     Ys = Y[Rt][:, Ct].double().cpu().numpy()
     # the GEMM alone: identical codes, levels and norms
     gstats = check_gemm(name + " gemm", Ys, oracle.qlinear(gx, gs, la, gw, gr, lw), gemm_scale(gx, gs, la, gw, gr, lw),

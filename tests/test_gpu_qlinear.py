@@ -1,5 +1,5 @@
 """GPU parity of the LUT-decode GEMM against the fp64 oracle contraction with identical codes
-and identical (fp16-rounded) levels: relative Frobenius error <= 2e-3 (fp32 accumulation
+and identical (bf16-rounded) levels: relative Frobenius error <= 2e-3 (fp32 accumulation
 leaves ~1e-6).  Codes and norms come from the seeded generator or from the oracle, never
 from the HIP path."""
 
@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2607_02461_amd as oq
 from paper_2607_02461_amd import workloads
-from tests.gpu_util import (GEMM_REL_F, check_gemm, gemm_scale, log_stats, near_tie_flip_bound, qlinear_oracle_fp16,
+from tests.gpu_util import (GEMM_REL_F, check_gemm, gemm_scale, log_stats, near_tie_flip_bound, qlinear_oracle_bf16,
                             rel_frobenius, to_f64)
 
 pytestmark = pytest.mark.gpu
@@ -27,9 +27,9 @@ def _inputs(M, N, K, ba, bw, seed):
 
 
 def _scale(xc, xs, ba, wc, wr, bw, K):
-    """Per-element unit s_n r'_i ||a_n|| ||b_i|| on the oracle's fp16 levels."""
-    la = oracle.fp16_round(oracle.lloydmax_codebook(ba, K).levels)
-    lw = oracle.fp16_round(oracle.lloydmax_codebook(bw, K).levels)
+    """Per-element unit s_n r'_i ||a_n|| ||b_i|| on the oracle's bf16 levels."""
+    la = oracle.bf16_round(oracle.lloydmax_codebook(ba, K).levels)
+    lw = oracle.bf16_round(oracle.lloydmax_codebook(bw, K).levels)
     return gemm_scale(xc, xs, la, wc, wr, lw)
 
 
@@ -51,7 +51,7 @@ def test_random_codes(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
     args = (xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
-    check_gemm(f"gemm random M={M} N={N} K={K} W{bw}A{ba}", Y, qlinear_oracle_fp16(*args), _scale(*args), K)
+    check_gemm(f"gemm random M={M} N={N} K={K} W{bw}A{ba}", Y, qlinear_oracle_bf16(*args), _scale(*args), K)
 
 
 # shapes with at least one 256x256 tile per compute unit (256) run the large-tile kernel; these
@@ -67,7 +67,7 @@ def test_random_codes_large_tiles(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
     args = (xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
-    ref = qlinear_oracle_fp16(*args)
+    ref = qlinear_oracle_bf16(*args)
     worst_row = float(np.max(np.linalg.norm(Y - ref, axis=1) / np.maximum(np.linalg.norm(ref, axis=1), 1e-300)))
     check_gemm(f"gemm large-tile M={M} N={N} K={K} W{bw}A{ba}", Y, ref, _scale(*args), K, worst_row_rel=worst_row)
     assert worst_row <= GEMM_REL_F
@@ -94,7 +94,7 @@ def test_fused_epilogue(M, N, K, bias, gelu, bf16, pad):
                             gelu=gelu, out_dtype=dt, out=out)
     torch.cuda.synchronize()
     Yn = Y.float().cpu().numpy().astype(np.float64)
-    base = qlinear_oracle_fp16(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
+    base = qlinear_oracle_bf16(xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
     ref = oracle.layer_epilogue(base, bias=b.double().numpy() if bias else None, gelu=gelu)
     err = rel_frobenius(Yn, ref)
     stats = {"rel_f": err}
@@ -133,8 +133,8 @@ def test_constant_codes_closed_form():
     xs = workloads.random_norms(M, 3, 0)
     wr = workloads.random_norms(N, 3, 1).to(torch.bfloat16)
     Y = _gpu(xc, xs, wc, wr, 4, 3, K)
-    la = cba.lut_f16.view(np.float16).astype(np.float64)
-    lw = cbw.lut_f16.view(np.float16).astype(np.float64)
+    la = (cba.lut_bf16.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    lw = (cbw.lut_bf16.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     want = xs.double().numpy()[:, None] * wr.double().numpy()[None, :] * K * la[13] * lw[2]
     assert np.max(np.abs(Y - want) / np.abs(want)) < 1e-5
 
@@ -157,9 +157,9 @@ def test_c4_up_shape_sampled_rows():
     rows = np.sort(np.random.default_rng(46).choice(M, 256, replace=False))
     rows[-1] = M - 1
     ridx = torch.as_tensor(rows, device=DEV)
-    ref = qlinear_oracle_fp16(xc[ridx].cpu().numpy(), xs[ridx].double().cpu().numpy(), 4,
+    ref = qlinear_oracle_bf16(xc[ridx].cpu().numpy(), xs[ridx].double().cpu().numpy(), 4,
                               wc.cpu().numpy(), wr.double().cpu().numpy(), 4, K)
-    la = oracle.fp16_round(oracle.lloydmax_codebook(4, K).levels)
+    la = oracle.bf16_round(oracle.lloydmax_codebook(4, K).levels)
     scale = gemm_scale(xc[ridx].cpu().numpy(), xs[ridx].double().cpu().numpy(), la, wc.cpu().numpy(),
                        wr.double().cpu().numpy(), la)
     check_gemm("gemm c4 up sampled", Y[ridx].double().cpu().numpy(), ref, scale, K, rows=len(rows))
@@ -184,7 +184,7 @@ def test_end_to_end_c1(bw, ba):
     oca, ocw = oracle.lloydmax_codebook(ba, K), oracle.lloydmax_codebook(bw, K)
     cx, s, Ux = oracle.quantize_act(Xd, oplan, oca)
     cw, r, Uw = oracle.quantize_weights(Wd, oplan, ocw)
-    la, lw = oracle.fp16_round(oca.levels), oracle.fp16_round(ocw.levels)
+    la, lw = oracle.bf16_round(oca.levels), oracle.bf16_round(ocw.levels)
     ref_q = oracle.qlinear(cx, s, la, cw, r, lw)
     dense = oracle.qlinear_dense_reference(Xd, Wd)
     Yn = Y.cpu().numpy().astype(np.float64)
@@ -234,7 +234,7 @@ def test_long_contraction(ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=K + ba)
     Y = _gpu(xc, xs, wc, wr, ba, bw, K)
     args = (xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
-    check_gemm(f"gemm long K={K} W{bw}A{ba}", Y, qlinear_oracle_fp16(*args), _scale(*args), K)
+    check_gemm(f"gemm long K={K} W{bw}A{ba}", Y, qlinear_oracle_bf16(*args), _scale(*args), K)
 
 
 def test_long_contraction_large_tiles_sampled_rows():
@@ -245,7 +245,7 @@ def test_long_contraction_large_tiles_sampled_rows():
     rows = np.sort(np.random.default_rng(9).choice(M, 64, replace=False))
     rows[-1] = M - 1
     args = (xc.numpy()[rows], xs.double().numpy()[rows], ba, wc.numpy(), wr.double().numpy(), bw, K)
-    check_gemm(f"gemm long large-tile K={K}", Y[rows], qlinear_oracle_fp16(*args), _scale(*args), K, rows=len(rows))
+    check_gemm(f"gemm long large-tile K={K}", Y[rows], qlinear_oracle_bf16(*args), _scale(*args), K, rows=len(rows))
 
 
 def test_empty_operands_are_noops():

@@ -11,7 +11,7 @@ import torch
 import oracle
 import paper_2607_02461_amd as oq
 from paper_2607_02461_amd import workloads
-from tests.gpu_util import GEMM_REL_F, check_gemm, gemm_scale, log_stats, qlinear_oracle_fp16, rel_frobenius
+from tests.gpu_util import GEMM_REL_F, check_gemm, gemm_scale, log_stats, qlinear_oracle_bf16, rel_frobenius
 
 pytestmark = pytest.mark.gpu
 
@@ -30,9 +30,9 @@ def _operands(M, N, K, ba, bw, seed):
 
 
 def _scale(xc, xs, ba, wc, wr, bw, K):
-    """Per-element unit s_n r'_i ||a_n|| ||b_i|| on the oracle's fp16 levels."""
-    la = oracle.fp16_round(oracle.lloydmax_codebook(ba, K).levels)
-    lw = oracle.fp16_round(oracle.lloydmax_codebook(bw, K).levels)
+    """Per-element unit s_n r'_i ||a_n|| ||b_i|| on the oracle's bf16 levels."""
+    la = oracle.bf16_round(oracle.lloydmax_codebook(ba, K).levels)
+    lw = oracle.bf16_round(oracle.lloydmax_codebook(bw, K).levels)
     return gemm_scale(xc, xs, la, wc, wr, lw)
 
 
@@ -65,7 +65,7 @@ def test_split_matches_oracle_and_unsplit(M, N, K, ba, bw):
     Y, Y0 = Y.cpu().numpy().astype(np.float64), Y0.cpu().numpy().astype(np.float64)
     xc, xsh, wc, wrh = host
     args = (xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
-    ref = qlinear_oracle_fp16(*args)
+    ref = qlinear_oracle_bf16(*args)
     err0, d = rel_frobenius(Y0, ref), rel_frobenius(Y, Y0)
     check_gemm(f"split M={M} N={N} K={K} W{bw}A{ba} splits={S}", Y, ref, _scale(*args), K, rel_f_unsplit=err0,
                vs_unsplit=d)
@@ -91,7 +91,7 @@ def test_split_tail_of_large_grid(M, N, K):
     xc, xsh, wc, wrh = host
     args = (xc.numpy()[rows], xsh.double().numpy()[rows], ba, wc.numpy(), wrh.double().numpy(), bw, K)
     d = rel_frobenius(Y, Y0)
-    check_gemm(f"split tail M={M} N={N} K={K} workspace={n}", Y[rows], qlinear_oracle_fp16(*args), _scale(*args), K,
+    check_gemm(f"split tail M={M} N={N} K={K} workspace={n}", Y[rows], qlinear_oracle_bf16(*args), _scale(*args), K,
                vs_unsplit=d)
     assert d <= 1e-5
 
@@ -108,7 +108,7 @@ def test_split_remaining_bit_pairs(M, N, K, ba, bw):
     xc, xsh, wc, wrh = host
     args = (xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
     check_gemm(f"split bits M={M} N={N} K={K} W{bw}A{ba}", Y.cpu().numpy().astype(np.float64),
-               qlinear_oracle_fp16(*args), _scale(*args), K)
+               qlinear_oracle_bf16(*args), _scale(*args), K)
 
 
 @pytest.mark.parametrize("bias,gelu,bf16", [(True, False, False), (False, True, False), (False, False, True),
@@ -129,7 +129,7 @@ def test_split_fused_epilogue(bias, gelu, bf16, pad):
     torch.cuda.synchronize()
     Yn = Y.float().cpu().numpy().astype(np.float64)
     xc, xsh, wc, wrh = host
-    base = qlinear_oracle_fp16(xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
+    base = qlinear_oracle_bf16(xc.numpy(), xsh.double().numpy(), ba, wc.numpy(), wrh.double().numpy(), bw, K)
     bd = b.double().numpy() if bias else None
     ref = oracle.layer_epilogue(base, bias=bd, gelu=gelu)
     if bf16:
@@ -177,7 +177,7 @@ def test_workspace_reused_across_shapes():
     torch.cuda.synchronize()
     for (xc, xsh, wc, wrh), K, Y in outs:
         args = (xc.numpy(), xsh.double().numpy(), 4, wc.numpy(), wrh.double().numpy(), 3, K)
-        check_gemm(f"split workspace reuse K={K}", Y.cpu().numpy().astype(np.float64), qlinear_oracle_fp16(*args),
+        check_gemm(f"split workspace reuse K={K}", Y.cpu().numpy().astype(np.float64), qlinear_oracle_bf16(*args),
                    _scale(*args), K)
 
 

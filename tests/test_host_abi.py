@@ -44,9 +44,9 @@ def test_codebook_matches_oracle(bits, d):
     # exact antisymmetry, middle threshold exactly zero
     assert np.array_equal(cb.levels, -cb.levels[::-1])
     assert cb.thresholds[(1 << bits) // 2 - 1] == 0.0
-    # the fp16 image equals round-to-nearest-even of the oracle's levels
-    want = ref.levels.astype(np.float16).view(np.uint16)
-    assert np.array_equal(cb.lut_f16, want)
+    # the bf16 image equals the oracle's levels rounded once to 8 significant bits, ties to even
+    want = oracle.bf16_bits(oracle.bf16_round(ref.levels))
+    assert np.array_equal(cb.lut_bf16, want)
 
 
 def test_codebook_d3_uniform_and_large_d():

@@ -11,7 +11,7 @@ import torch
 import oracle
 import paper_2607_02461_amd as oq
 from paper_2607_02461_amd import workloads
-from tests.gpu_util import check_gemm, gemm_scale, qlinear_oracle_fp16
+from tests.gpu_util import check_gemm, gemm_scale, qlinear_oracle_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -33,9 +33,9 @@ def _operands(M, N, K, ba, bw, seed):
 def _oracle_check(name, Y, host, ba, bw, K):
     xc, xs, wc, wr = host
     args = (xc.numpy(), xs.double().numpy(), ba, wc.numpy(), wr.double().numpy(), bw, K)
-    la = oracle.fp16_round(oracle.lloydmax_codebook(ba, K).levels)
-    lw = oracle.fp16_round(oracle.lloydmax_codebook(bw, K).levels)
-    check_gemm(name, Y.cpu().numpy().astype(np.float64), qlinear_oracle_fp16(*args),
+    la = oracle.bf16_round(oracle.lloydmax_codebook(ba, K).levels)
+    lw = oracle.bf16_round(oracle.lloydmax_codebook(bw, K).levels)
+    check_gemm(name, Y.cpu().numpy().astype(np.float64), qlinear_oracle_bf16(*args),
                gemm_scale(args[0], args[1], la, args[3], args[4], lw), K)
 
 
