@@ -685,9 +685,12 @@ def rotation_per_image(oq, dev, reps):
 def trunk_sweep(oq, workloads, dev, steps, warmup=1):
     """The video-DiT trunk sweep: per denoising step, the activation quantizer and the GEMM of
     every linear of 40 blocks (QKV, out, FFN up, FFN down at M = 32760), summed over the 160
-    calls; and the offline weight pass over all 160 weight matrices, their 160 launches timed back
-    to back with the weights' generation outside the timing.  One activation draw per input width
-    serves every block."""
+    calls; and the offline weight pass over all 160 weight matrices.  Every layer of input width d
+    shares the one rotation Pi_d (Sec. 4.2), so the weight rows of one width form one row set: the
+    pass quantizes it in one launch per width (two here), each matrix's codes and norms being a row
+    range of the result.  The same pass as 160 launches, one per matrix, is timed beside it.
+    Weights are generated outside the timing.  One activation draw per input width serves every
+    block."""
     wl = workloads.C5
     acts = workloads.c5_acts(device=dev)
     M = workloads.C5_M
@@ -697,28 +700,53 @@ def trunk_sweep(oq, workloads, dev, steps, warmup=1):
     xn = {K: torch.empty((M,), dtype=torch.float32, device=dev) for K in acts}
     Yflat = torch.empty(max(M * lin.N for lin in wl.linears), dtype=torch.float32, device=dev)
 
-    # offline weight pass over all blocks: the 160 bf16 weight matrices (19.7 GB) are generated
-    # first, then quantized back to back between one pair of events (generation outside the
-    # timing), then freed
-    wcodes, wnorms, Ws, lins = [], [], [], []
-    wp_bytes, n_weights = 0.0, 0
+    # the 160 bf16 weight matrices (19.7 GB) as row ranges of one [rows, d] buffer per width
+    rows = {K: 0 for K in acts}
+    spans = []
     for b in range(wl.repeat):
         for li, lin in enumerate(wl.linears):
-            Ws.append(workloads.c5_weight(b, li, device=dev))
-            lins.append(lin)
-            wcodes.append(torch.empty((lin.N, lin.K // 2), dtype=torch.uint8, device=dev))
-            wnorms.append(torch.empty((lin.N,), dtype=torch.bfloat16, device=dev))
-            wp_bytes += lin.N * (2 * lin.K + lin.K // 2 + 2)
-            n_weights += lin.N * lin.K
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            spans.append((lin, rows[lin.K], rows[lin.K] + lin.N))
+            rows[lin.K] += lin.N
+    Wcat = {K: torch.empty((n, K), dtype=torch.bfloat16, device=dev) for K, n in rows.items()}
+    ccat = {K: torch.empty((n, K // 2), dtype=torch.uint8, device=dev) for K, n in rows.items()}
+    ncat = {K: torch.empty((n,), dtype=torch.bfloat16, device=dev) for K, n in rows.items()}
+    for i, (lin, r0, r1) in enumerate(spans):
+        b, li = divmod(i, len(wl.linears))
+        Wcat[lin.K][r0:r1].copy_(workloads.c5_weight(b, li, device=dev))
+    wcodes = [ccat[lin.K][r0:r1] for lin, r0, r1 in spans]
+    wnorms = [ncat[lin.K][r0:r1] for lin, r0, r1 in spans]
+    wp_bytes = float(sum(n * (2 * K + K // 2 + 2) for K, n in rows.items()))
+    n_weights = sum(n * K for K, n in rows.items())
+
+    def timed(fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1)
+
+    def batched():
+        for K in rows:
+            oq.quantize_weights_offline(plans[K], cbs[K], Wcat[K], 1e-10, ccat[K], ncat[K])
+
+    def per_matrix():
+        for lin, r0, r1 in spans:
+            oq.quantize_weights_offline(plans[lin.K], cbs[lin.K], Wcat[lin.K][r0:r1], 1e-10, ccat[lin.K][r0:r1],
+                                        ncat[lin.K][r0:r1])
+
+    # an untimed pass first: the first writes into freshly allocated output memory are several
+    # times slower than later ones.  Then the pass as one launch per matrix (its results checked
+    # against the untimed pass), and twice as one launch per width.
+    batched()
     torch.cuda.synchronize()
-    e0.record()
-    for W, lin, wc, wn in zip(Ws, lins, wcodes, wnorms):
-        oq.quantize_weights_offline(plans[lin.K], cbs[lin.K], W, 1e-10, wc, wn)
-    e1.record()
-    torch.cuda.synchronize()
-    wp_ms = e0.elapsed_time(e1)
-    del Ws
+    ref = {K: (ccat[K].clone(), ncat[K].clone()) for K in rows}
+    per_matrix_ms = timed(per_matrix)
+    same = all(torch.equal(ref[K][0], ccat[K]) and torch.equal(ref[K][1], ncat[K]) for K in rows)
+    wp_runs = [timed(batched) for _ in range(2)]
+    wp_ms = float(np.mean(wp_runs))
+    del Wcat, ref
 
     def step(ev=None):
         for b in range(wl.repeat):
@@ -758,6 +786,12 @@ def trunk_sweep(oq, workloads, dev, steps, warmup=1):
             "quant_ms_sum": q_ms, "quant_gbs": qbytes / (q_ms * 1e-3) / 1e9,
             "quant_frac_of_hbm": qbytes / (q_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "weight_pass_ms": wp_ms, "weight_pass_gbs": wp_bytes / (wp_ms * 1e-3) / 1e9,
+            "weight_pass_frac_of_hbm": wp_bytes / (wp_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "weight_pass_launches": len(rows), "weight_pass_runs_ms": wp_runs,
+            "weight_pass_rows": {str(K): n for K, n in rows.items()},
+            "weight_pass_per_matrix": {"launches": len(spans), "ms": per_matrix_ms,
+                                       "gbs": wp_bytes / (per_matrix_ms * 1e-3) / 1e9,
+                                       "codes_and_norms_equal": bool(same)},
             "weights": n_weights, "weight_code_bytes": int(sum(c.numel() for c in wcodes))}
 
 

@@ -46,6 +46,37 @@ constexpr int kLaneVals = 16;   // positions per lane
 // 1024 bytes further (an immediate offset of the LDS instructions).
 constexpr int kBufGap = 1024;
 
+// Butterfly between lanes 16 (SPAN = 16) or 32 (SPAN = 32) apart on two registers at once, with
+// v_permlane16_swap / v_permlane32_swap (VALU, no LDS).  The swap trades the upper SPAN lanes of
+// each 2*SPAN group of `a` for the lower SPAN lanes of `b`, so each lane then holds a pair
+// (x_lo, x_hi) of one register; it forms x_lo + x_hi and x_hi - x_lo, and a second swap puts both
+// back where they belong: a lower lane ends with x_lo + x_hi, an upper one with x_hi - x_lo, as a
+// fused multiply-add own + (-1 on upper lanes) partner would give.
+template <int SPAN>
+__device__ __forceinline__ void swap_butterfly(float& a, float& b) {
+    static_assert(SPAN == 16 || SPAN == 32, "span");
+    uint32_t lo, hi;
+    if constexpr (SPAN == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+        lo = r[0];
+        hi = r[1];
+    } else {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+        lo = r[0];
+        hi = r[1];
+    }
+    const float s = __uint_as_float(lo) + __uint_as_float(hi), d = __uint_as_float(hi) - __uint_as_float(lo);
+    if constexpr (SPAN == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(s), __float_as_uint(d), false, false);
+        a = __uint_as_float(r[0]);
+        b = __uint_as_float(r[1]);
+    } else {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(s), __float_as_uint(d), false, false);
+        a = __uint_as_float(r[0]);
+        b = __uint_as_float(r[1]);
+    }
+}
+
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float v) {
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
@@ -243,8 +274,8 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
     // Stages across lanes.  An h-block (h = 128 * 2^OUTER) spans L = h/16 consecutive, aligned lanes
     // and its Hadamard stages pair lane j with j ^ v along a basis of the lane-index bits:
     //   h = 128:   v = 1, 2 (quad_perm), 7 (row_half_mirror)                          dual {5, 6, 4}
-    //   h >= 256:  v = 1, 2, 7, 15 (row_mirror), then 16 (ds_swizzle) and 32 (ds_bpermute) as far
-    //              as the block spans                                                  dual {5, 6, 12, 8, 16, 32}
+    //   h >= 256:  v = 1, 2, 7, 15 (row_mirror), then 16 and 32 (lane swaps) as far as the block
+    //              spans                                                               dual {5, 6, 12, 8, 16, 32}
     // Butterflies along a basis v_k whose lower / upper roles follow the dual basis s_k (parity of
     // s_k & v_m is 1 iff k = m) compute the Sylvester transform with permuted outputs: lane j ends
     // with the 16 outputs of lane position M(j), the XOR of the s_k whose parity with j is odd, so
@@ -255,7 +286,7 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
     const int j = tid & (LB - 1);
     constexpr int d1 = 5, d2 = 6, d3 = OUTER == 0 ? 4 : 12, d4 = 8;
     const float sg1 = odd(j & d1) ? -1.f : 1.f, sg2 = odd(j & d2) ? -1.f : 1.f, sg3 = odd(j & d3) ? -1.f : 1.f;
-    const float sg4 = odd(j & d4) ? -1.f : 1.f, sg5 = (j & 16) ? -1.f : 1.f, sg6 = (j & 32) ? -1.f : 1.f;
+    const float sg4 = odd(j & d4) ? -1.f : 1.f;
     int mj = (odd(j & d1) ? d1 : 0) ^ (odd(j & d2) ? d2 : 0) ^ (odd(j & d3) ? d3 : 0);
     if (OUTER >= 1 && odd(j & d4)) mj ^= d4;
     mj |= j & ~15;                                         // bits 4, 5: the standard basis
@@ -292,7 +323,7 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
 
     // staging: wave w brings chunks 64 w + 64 v .. 64 w + 64 v + 63 of a row for v = 0, T/64, ...
     // (T threads), straight from HBM into LDS (global_load_lds_dwordx4: lane i of the wave writes
-    // the LDS base + 16 i); the loads complete before the iteration's barrier
+    // the LDS base + 16 i); a row issued after one barrier has landed by the next
     const int G = gridDim.x;
     const int M = (int)p.M;   // below 2^31 (checked by the caller)
     const int nchunks = p.K / 8, wave = tid >> 6, waves = blockDim.x >> 6;
@@ -316,10 +347,13 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
         }
     };
 
+    // The first row, then the second in flight before the loop (the loop keeps one row in flight
+    // for a whole iteration: issued right after a barrier, waited for at the next one).
     int g = blockIdx.x;
     if (g < M) load_row(g, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    load_row(g + G, 1);
 
     const float cm = p.enc_center + 8388608.0f;
     // f = C + 2^23 + round(t - C) has the bit pattern 0x4B000000 + cell, so the cell's LDS byte
@@ -328,12 +362,10 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
     const int64_t code_row = (int64_t)p.K * BITS / 8;
 
     // One row from staging buffer BUF (a compile-time constant, so the buffer offset is the LDS
-    // instructions' immediate): the loop below alternates the two.
+    // instructions' immediate): the loop below alternates the two.  Row g + G is already in flight
+    // into the other buffer.
     auto iteration = [&](auto buf_tag) {
         constexpr int BUF = decltype(buf_tag)::value;
-        // row g + G into the other buffer, whose last reader was row g - G, before the previous
-        // barrier
-        load_row(g + G, BUF ^ 1);
         // gather: pair i = positions 2i (low half), 2i+1 (high half).  All sixteen reads are issued
         // before the first is used (one LDS round trip per row, not two).
         uint16_t gv[kLaneVals];
@@ -366,26 +398,14 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
         ORBIT_ROW_DPP16(z, sg2, "quad_perm:[2,3,0,1]");
         ORBIT_ROW_DPP16(z, sg3, "row_half_mirror");
         if constexpr (OUTER >= 1) ORBIT_ROW_DPP16(z, sg4, "row_mirror");
-        // lanes 16 apart inside 32 (swizzle, bit mode: xor 16), then 32 apart (bpermute), eight
-        // registers at a time so that the exchanges in flight need few temporaries
+        // lanes 16 apart inside 32, then 32 apart: register pairs through lane swaps
         if constexpr (OUTER >= 2) {
 #pragma unroll
-            for (int c = 0; c < kLaneVals; c += 8) {
-#pragma unroll
-                for (int r = c; r < c + 8; ++r)
-                    z[r] = fmaf(__int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(z[r]), 0x401F)), sg5, z[r]);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            for (int r = 0; r < kLaneVals; r += 2) swap_butterfly<16>(z[r], z[r + 1]);
         }
         if constexpr (OUTER >= 3) {
 #pragma unroll
-            for (int c = 0; c < kLaneVals; c += 8) {
-#pragma unroll
-                for (int r = c; r < c + 8; ++r)
-                    z[r] = fmaf(__int_as_float(__builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, __float_as_int(z[r]))), sg6,
-                                z[r]);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            for (int r = 0; r < kLaneVals; r += 2) swap_butterfly<32>(z[r], z[r + 1]);
         }
 
         // block sums of squares: the eight lanes of a block, in a fixed order
@@ -395,8 +415,11 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
         ss += dpp_mov<0x141>(ss);  // row_half_mirror
         float* const pt = part + BUF * nb;
         if (active && q == 0) pt[blk] = ss;
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the next row's staging loads
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // row g + G's staging loads
         __syncthreads();
+        // every wave has gathered row g: row g + 2G goes into its buffer, with the encode below and
+        // the next row's gather and transform to complete in
+        load_row(g + 2 * G, BUF);
         // row total: every wave sums the block partials in the same fixed order
         float acc = lane < nb ? pt[lane] : 0.f;   // nb <= 128 block partials
         if (lane + 64 < nb) acc += pt[lane + 64];
