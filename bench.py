@@ -942,8 +942,8 @@ def parity_vs_oracle(oracle, layers, prepared, last, gemm_rows=256, band=1e-5):
     res = []
     for L, (lin, plan, cba, cbw, cw, r, X), (cx, s, Ux) in zip(layers, prepared, last):
         n = X.shape[0]
-        gx = oracle.unpack_codes(L["xc"][:n].cpu().numpy(), lin.ba, lin.K)
-        gw = oracle.unpack_codes(L["wc"].cpu().numpy(), lin.bw, lin.K)
+        gx = oracle.from_labels(oracle.unpack_codes(L["xc"][:n].cpu().numpy(), lin.ba, lin.K), lin.ba)
+        gw = oracle.from_labels(oracle.unpack_codes(L["wc"].cpu().numpy(), lin.bw, lin.K), lin.bw)
         _, _, Uw = L.pop("_oracle_w")
         entry = {"linear": lin.name, "act_rows": n, "weight_rows": lin.N}
         for tag, g, c, U, th in (("act", gx, cx, Ux, cba.thresholds), ("weights", gw, cw, Uw, cbw.thresholds)):

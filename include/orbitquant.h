@@ -17,7 +17,12 @@
  *   - Matrices are row-major with the reduction dimension K contiguous.
  *   - Packed codes: an LSB-first bit stream per row; the code of coordinate k occupies bits
  *     [k*b, k*b + b) of the row, so a row of K codes is K*b/8 bytes and rows are contiguous.
- *     A code is the index of its level in the ascending level list (0 = most negative).
+ *     A code is stored as the sign-magnitude label of its level: with levels ascending and
+ *     antisymmetric (index c and 2^b - 1 - c are negatives of each other), level index
+ *     c >= 2^(b-1) (a positive level) is stored as c - 2^(b-1) and index c < 2^(b-1) as
+ *     2^b - 1 - c.  The label's top bit is the level's sign and its low b-1 bits rank the
+ *     level's magnitude (0 = nearest zero); the labels are a storage format and change no
+ *     nearest-level decision (Eq. (3)).
  *   - Device calls take device pointers the caller owns (e.g. torch tensors), only enqueue
  *     work on `stream` (a hipStream_t; NULL = the null stream) and return before it runs.
  *     They allocate no device memory for their operands.  Argument checks are synchronous

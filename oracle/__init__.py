@@ -28,7 +28,7 @@ from .plan import SplitMix64, rpbh_plan, Plan
 from .rpbh import rpbh_forward, rpbh_inverse, sylvester_hadamard, fwht_blocks
 from .quantize import (normalize_rows, encode, decode_levels, pack_codes, unpack_codes,
                        quantize_act, quantize_weights, near_tie_mask, nearest_threshold, bf16_round, bf16_bits,
-                       fp16_round)
+                       fp16_round, to_labels, from_labels)
 from .qlinear import layer_epilogue, qlinear, qlinear_dense_reference
 from .adaln_rtn import rtn_int4_quantize, rtn_int4_dequantize, pack_rtn_int4, unpack_rtn_int4, rtn_int4_linear
 
@@ -39,7 +39,7 @@ __all__ = [
     "lloydmax_codebook", "Codebook", "SplitMix64", "rpbh_plan", "Plan",
     "rpbh_forward", "rpbh_inverse", "sylvester_hadamard", "fwht_blocks",
     "normalize_rows", "encode", "decode_levels", "pack_codes", "unpack_codes",
-    "quantize_act", "quantize_weights", "near_tie_mask", "nearest_threshold", "bf16_round", "bf16_bits", "fp16_round",
+    "quantize_act", "quantize_weights", "near_tie_mask", "nearest_threshold", "bf16_round", "bf16_bits", "fp16_round", "to_labels", "from_labels",
     "qlinear", "qlinear_dense_reference", "EPS_DEFAULT",
     "rtn_int4_quantize", "rtn_int4_dequantize", "pack_rtn_int4", "unpack_rtn_int4", "rtn_int4_linear",
 ]

@@ -15,6 +15,10 @@ Readings taken where the paper is silent:
     code = #{j : tau_j <= u}.  Codes index the ascending levels (0 = most negative).
   * Packing is an LSB-first bit stream per row: code k occupies bits
     [k*b, k*b + b) of the row, so a row of K codes is K*b/8 bytes.
+  * Stored codes are sign-magnitude labels of the level index (the paper fixes no
+    storage labels): index c >= 2^(b-1) (a positive level) is stored as c - 2^(b-1),
+    index c < 2^(b-1) as 2^b - 1 - c.  The label's top bit is the sign of the level and
+    its low bits rank |level|; to_labels / from_labels convert.
 """
 
 import numpy as np
@@ -74,6 +78,20 @@ def nearest_threshold(U: np.ndarray, thresholds: np.ndarray) -> np.ndarray:
     lo = np.clip(idx - 1, 0, len(t) - 1)
     hi = np.clip(idx, 0, len(t) - 1)
     return np.where(np.abs(U - t[lo]) <= np.abs(U - t[hi]), lo, hi)
+
+
+def to_labels(codes, bits: int) -> np.ndarray:
+    """Level indices (0 = most negative level) -> stored sign-magnitude labels."""
+    c = np.asarray(codes, dtype=np.int64)
+    half = 1 << (bits - 1)
+    return np.where(c >= half, c - half, (2 * half - 1) - c)
+
+
+def from_labels(labels, bits: int) -> np.ndarray:
+    """Stored sign-magnitude labels -> level indices (the inverse of to_labels)."""
+    lab = np.asarray(labels, dtype=np.int64)
+    half = 1 << (bits - 1)
+    return np.where(lab < half, lab + half, (2 * half - 1) - lab)
 
 
 def decode_levels(codes: np.ndarray, levels: np.ndarray) -> np.ndarray:

@@ -72,9 +72,22 @@ struct QuantParams {
     uint32_t part_off, row_off, neg_off;
 };
 
+// Stored code labels.  A b-bit code of level index c (levels ascending) is stored as the
+// sign-magnitude label: c - 2^(b-1) for the upper half (positive levels) and 2^b - 1 - c for the
+// lower half, so the top bit is the level's sign and the low b-1 bits rank its magnitude.  On a
+// word of packed fields whose top bits are TOP, SHIFT = b - 1 apart from each field's bit 0, and
+// whose bits are MASK: t - (t >> SHIFT) is 2^(b-1) - 1 in fields with the top bit set (no borrow
+// leaves a field), so ~x ^ that is c - 2^(b-1) there and 2^b - 1 - c elsewhere.
+template <uint32_t TOP, int SHIFT, uint32_t MASK>
+__device__ __forceinline__ uint32_t sign_magnitude_labels(uint32_t x) {
+    const uint32_t t = x & TOP;
+    return (~x ^ (t - (t >> SHIFT))) & MASK;
+}
+
 int quant_rows_per_group(int K);
 // The one-row-per-workgroup quantizer (16 positions per lane) covers permutation plans with
-// h = 128 and K a multiple of 128 from 1024 to 16384; the general kernel covers the rest.
+// h = 128 .. 1024 and K a multiple of 128 and of h from 1024 to 16384; the general kernel covers
+// the rest.  Its persistent grid holds as many workgroups as are resident at once.
 bool rpbh_quantize_row_fits(int K, int h, bool gather);
 hipError_t launch_rpbh_quantize_row(QuantParams p, int bits, bool norm_bf16, int cus, hipStream_t stream);
 // gather: apply the permutation through the LDS-staged gather (false only for the identity).

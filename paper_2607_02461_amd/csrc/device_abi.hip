@@ -365,14 +365,20 @@ orbit_status orbit_qlinear_ws(orbit_codebook cb_a, const uint8_t* x_codes, const
     else
         g.splits = 1;
     for (const orbit_codebook_s* cb : {cb_a, cb_w}) {
-        // the 4-bit decoder reads the positive half and mirrors it
+        // the 4-bit decoder reads the positive half and takes the sign from the label's top bit
         if (cb->bits != 4) continue;
         for (int c = 0; c < 8; ++c)
             if (cb->lut_bf16[15 - c] != (uint16_t)(cb->lut_bf16[c] ^ 0x8000u))
                 return fail(ORBIT_EINTERNAL, "orbit_qlinear: 4-bit bf16 levels are not antisymmetric");
     }
-    for (int j = 0; j < 64; ++j) g.lut_a[j] = j < (1 << cb_a->bits) ? cb_a->lut_bf16[j] : 0;
-    for (int j = 0; j < 16; ++j) g.lut_w[j] = j < (1 << cb_w->bits) ? cb_w->lut_bf16[j] : 0;
+    // the levels in label order: label l < 2^(b-1) is level index 2^(b-1) + l, label l above that
+    // is level index 2^b - 1 - l
+    auto by_label = [](const orbit_codebook_s* cb, int l) -> uint16_t {
+        const int n = 1 << cb->bits, half = n / 2;
+        return cb->lut_bf16[l < half ? half + l : n - 1 - l];
+    };
+    for (int j = 0; j < 64; ++j) g.lut_a[j] = j < (1 << cb_a->bits) ? by_label(cb_a, j) : 0;
+    for (int j = 0; j < 16; ++j) g.lut_w[j] = j < (1 << cb_w->bits) ? by_label(cb_w, j) : 0;
     hipError_t e = launch_lut_gemm(g, cb_a->bits, cb_w->bits, info.cus, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "orbit_qlinear");
     return ORBIT_OK;

@@ -38,13 +38,14 @@ struct ByteTables {
     uint32_t lo[2], hi[2];  // byte e of lo[e/4] (hi[e/4]) is the low (high) byte of table entry e
 };
 
-// Tables of at most eight levels hold every level.  The 4-bit table holds the positive half
-// L[8..15] only: the codebook is antisymmetric (L[15-c] = -L[c], Sec. 3's symmetric marginal),
-// so a code below 8 reads the mirrored entry and sets the bf16 sign bit.  The host checks the
-// antisymmetry bit for bit before launching.
+// `lut` holds the levels in label order (entry l is the level of sign-magnitude label l).  Tables
+// of at most eight levels hold every label.  The 4-bit table holds labels 0..7 only, the positive
+// levels by rank: the codebook is antisymmetric (L[15-c] = -L[c], Sec. 3's symmetric marginal),
+// so label 8 + m is the negation of label m, and the decoder looks up the low three bits and
+// moves bit 3 into the bf16 sign bit.  The host checks the antisymmetry bit for bit.
 template <int BITS>
 __device__ __forceinline__ ByteTables make_tables(const uint16_t* lut) {
-    constexpr int n = BITS == 4 ? 8 : BITS == 6 ? 0 : 1 << BITS, first = BITS == 4 ? 8 : 0;
+    constexpr int n = BITS == 4 ? 8 : BITS == 6 ? 0 : 1 << BITS, first = 0;
     ByteTables t;
 #pragma unroll
     for (int w = 0; w < 2; ++w) {
@@ -134,19 +135,16 @@ __device__ __forceinline__ void decode8(const Codes<BITS>& w, int g, const ByteT
     if constexpr (BITS == 6) {
         decode8_lds6(w, g, tab6, out);
     } else if constexpr (BITS == 4) {
-        // nibble j of x is code k_j; neg has bit 3 of each nibble set where that code is below 8
-        // (a negative level); there the low three bits are mirrored (j -> 7 - j) to index the
-        // positive half, and the sign bit is set on the high byte afterwards.  The empty asm pins
-        // the decode here: otherwise the compiler starts it right after the codes' load, which
-        // then has to complete a whole K-step early.
+        // nibble j of x is the label of code k_j: bits 0-2 index the magnitude table, bit 3 (the
+        // sign) becomes bit 7 of the high byte, where bf16 keeps its sign.  The empty asm pins the
+        // decode here: otherwise the compiler starts it right after the codes' load, which then
+        // has to complete a whole K-step early.
         uint32_t x = w[g];
         asm volatile("" : "+v"(x));
-        const uint32_t neg = ~x & 0x88888888u;
-        const uint32_t idx = x ^ (neg - (neg >> 3));
-        lookup_bytes(idx & 0x07070707u, t, lo, hi);                  // k0 k2 k4 k6
-        interleave(lo, hi | ((neg << 4) & 0x80808080u), out[0], out[1]);
-        lookup_bytes((idx >> 4) & 0x07070707u, t, lo, hi);           // k1 k3 k5 k7
-        interleave(lo, hi | (neg & 0x80808080u), out[2], out[3]);
+        lookup_bytes(x & 0x07070707u, t, lo, hi);                  // k0 k2 k4 k6
+        interleave(lo, hi | ((x << 4) & 0x80808080u), out[0], out[1]);
+        lookup_bytes((x >> 4) & 0x07070707u, t, lo, hi);           // k1 k3 k5 k7
+        interleave(lo, hi | (x & 0x80808080u), out[2], out[3]);
     } else {
         decode8_small<BITS>(w, g, t, out);
     }

@@ -171,9 +171,10 @@ __device__ __forceinline__ uint32_t code_byte(float y, uint32_t into) {
     return __builtin_amdgcn_cvt_pk_u8_f32(y, K, into);
 }
 
-// Packs 32 codes, given as values y whose nearest integer is the code, LSB-first into 4*BITS
-// bytes.  v_cvt_pk_u8_f32 converts a value and inserts it as one byte of a word in a single op;
-// the codes are spread over bytes so that a few shifts and ORs close the gaps between them.
+// Packs 32 codes, given as values y whose nearest integer is the level index, as sign-magnitude
+// labels LSB-first into 4*BITS bytes.  v_cvt_pk_u8_f32 converts a value and inserts it as one byte
+// of a word in a single op; the codes are spread over bytes so that a few shifts and ORs close the
+// gaps between them, and the labels are formed on words of byte or packed fields.
 template <int BITS>
 __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[6]) {
     if constexpr (BITS == 6) {
@@ -186,7 +187,7 @@ __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[6
             uint32_t A = code_byte<0>(v[0], 0u);
             A = code_byte<1>(v[1], A);
             A = code_byte<2>(v[2], A);
-            A = code_byte<3>(v[3], A);
+            A = sign_magnitude_labels<0x20202020u, 5, 0x3F3F3F3Fu>(code_byte<3>(v[3], A));
             g[i] = (A & 0x3Fu) | ((A >> 2) & 0xFC0u) | ((A >> 4) & 0x3F000u) | ((A >> 6) & 0xFC0000u);
         }
 #pragma unroll
@@ -208,7 +209,7 @@ __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[6
             B = code_byte<2>(v[5], B);
             A = code_byte<3>(v[6], A);
             B = code_byte<3>(v[7], B);
-            w[i] = A | (B << 4);
+            w[i] = sign_magnitude_labels<0x88888888u, 3, 0xFFFFFFFFu>(A | (B << 4));
         }
         return;
     } else if constexpr (BITS == 2) {
@@ -224,7 +225,7 @@ __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[6
                 d = code_byte<2>(v[8 + k], d);
                 D[k] = code_byte<3>(v[12 + k], d);
             }
-            w[i] = D[0] | (D[1] << 2) | (D[2] << 4) | (D[3] << 6);
+            w[i] = sign_magnitude_labels<0xAAAAAAAAu, 1, 0xFFFFFFFFu>(D[0] | (D[1] << 2) | (D[2] << 4) | (D[3] << 6));
         }
         w[2] = w[3] = w[4] = w[5] = 0u;
     } else {
@@ -241,7 +242,7 @@ __device__ __forceinline__ void pack_codes(const float (&y)[32], uint32_t (&w)[6
             B = code_byte<2>(v[5], B);
             A = code_byte<3>(v[6], A);
             B = code_byte<3>(v[7], B);
-            const uint32_t P = A | (B << 3);
+            const uint32_t P = sign_magnitude_labels<0x24242424u, 2, 0x3F3F3F3Fu>(A | (B << 3));
             g[i] = (P & 0x3Fu) | ((P >> 2) & 0xFC0u) | ((P >> 4) & 0x3F000u) | ((P >> 6) & 0xFC0000u);
         }
         w[0] = g[0] | (g[1] << 24);

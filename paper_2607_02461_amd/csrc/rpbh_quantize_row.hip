@@ -171,8 +171,10 @@ __device__ __forceinline__ uint32_t code_byte(float y, uint32_t into) {
     return __builtin_amdgcn_cvt_pk_u8_f32(y, K, into);
 }
 
-// 16 codes, given as values y whose nearest integer is the code, packed LSB-first into 2*BITS
-// bytes: w[0] (2 bits), w[0..1] (4 bits), w[0] and the low half of w[1] (3 bits), w[0..2] (6 bits).
+// 16 codes, given as values y whose nearest integer is the level index, stored as sign-magnitude
+// labels packed LSB-first into 2*BITS bytes: w[0] (2 bits), w[0..1] (4 bits), w[0] and the low
+// half of w[1] (3 bits), w[0..2] (6 bits).  The labels are formed on words of byte or packed
+// fields (one bitwise pass per word).
 template <int BITS>
 __device__ __forceinline__ void pack16(const float (&y)[16], uint32_t (&w)[3]) {
     if constexpr (BITS == 4) {
@@ -187,7 +189,7 @@ __device__ __forceinline__ void pack16(const float (&y)[16], uint32_t (&w)[3]) {
             B = code_byte<2>(v[5], B);
             A = code_byte<3>(v[6], A);
             B = code_byte<3>(v[7], B);
-            w[i] = A | (B << 4);
+            w[i] = sign_magnitude_labels<0x88888888u, 3, 0xFFFFFFFFu>(A | (B << 4));
         }
         w[2] = 0u;
     } else if constexpr (BITS == 2) {
@@ -200,7 +202,7 @@ __device__ __forceinline__ void pack16(const float (&y)[16], uint32_t (&w)[3]) {
             d = code_byte<2>(y[8 + k], d);
             D[k] = code_byte<3>(y[12 + k], d);
         }
-        w[0] = D[0] | (D[1] << 2) | (D[2] << 4) | (D[3] << 6);
+        w[0] = sign_magnitude_labels<0xAAAAAAAAu, 1, 0xFFFFFFFFu>(D[0] | (D[1] << 2) | (D[2] << 4) | (D[3] << 6));
         w[1] = w[2] = 0u;
     } else if constexpr (BITS == 3) {
         // 8 codes = 24 bits: codes 2j, 2j+1 share byte j of P (6 bits), then the gaps close
@@ -215,7 +217,7 @@ __device__ __forceinline__ void pack16(const float (&y)[16], uint32_t (&w)[3]) {
             B = code_byte<2>(v[5], B);
             A = code_byte<3>(v[6], A);
             B = code_byte<3>(v[7], B);
-            const uint32_t P = A | (B << 3);
+            const uint32_t P = sign_magnitude_labels<0x24242424u, 2, 0x3F3F3F3Fu>(A | (B << 3));
             g[i] = (P & 0x3Fu) | ((P >> 2) & 0xFC0u) | ((P >> 4) & 0x3F000u) | ((P >> 6) & 0xFC0000u);
         }
         w[0] = g[0] | (g[1] << 24);  // bytes 0..3
@@ -231,7 +233,7 @@ __device__ __forceinline__ void pack16(const float (&y)[16], uint32_t (&w)[3]) {
             uint32_t A = code_byte<0>(v[0], 0u);
             A = code_byte<1>(v[1], A);
             A = code_byte<2>(v[2], A);
-            A = code_byte<3>(v[3], A);
+            A = sign_magnitude_labels<0x20202020u, 5, 0x3F3F3F3Fu>(code_byte<3>(v[3], A));
             g[i] = (A & 0x3Fu) | ((A >> 2) & 0xFC0u) | ((A >> 4) & 0x3F000u) | ((A >> 6) & 0xFC0000u);
         }
         w[0] = g[0] | (g[1] << 24);

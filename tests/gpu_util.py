@@ -73,7 +73,7 @@ def compare_quantizer(name, X: torch.Tensor, bits: int, seed: int = 0, weights: 
     else:
         oc, on, U = oracle.quantize_act(Xs, oplan, ocb, eps)
     gcodes = codes.cpu().numpy()[sel]
-    gc = oracle.unpack_codes(gcodes, bits, K)
+    gc = oracle.from_labels(oracle.unpack_codes(gcodes, bits, K), bits)
     cstats = code_stats(gc, oc, U, ocb.thresholds)
     if weights:
         gn = norms.float().cpu().numpy().astype(np.float64)[sel]

@@ -28,7 +28,7 @@ def _sample(n, count, seed):
 
 
 def _check_codes(name, gpu_codes, bits, K, oc, U, thresholds):
-    gc = oracle.unpack_codes(gpu_codes, bits, K)
+    gc = oracle.from_labels(oracle.unpack_codes(gpu_codes, bits, K), bits)
     stats = code_stats(gc, oc, U, thresholds)
     assert_codes(name, stats)
     return gc, stats

@@ -35,8 +35,8 @@ def _scale(xc, xs, ba, wc, wr, bw, K):
 
 def _gpu(xc, xs, wc, wr, ba, bw, K):
     cba, cbw = oq.lloydmax_codebook(ba, K), oq.lloydmax_codebook(bw, K)
-    xp = torch.from_numpy(oracle.pack_codes(xc.numpy(), ba)).to(DEV)
-    wp = torch.from_numpy(oracle.pack_codes(wc.numpy(), bw)).to(DEV)
+    xp = torch.from_numpy(oracle.pack_codes(oracle.to_labels(xc.numpy(), ba), ba)).to(DEV)
+    wp = torch.from_numpy(oracle.pack_codes(oracle.to_labels(wc.numpy(), bw), bw)).to(DEV)
     Y = oq.orbit_qlinear(cba, xp, xs.to(DEV), cbw, wp, wr.to(DEV))
     torch.cuda.synchronize()
     return Y.cpu().numpy().astype(np.float64)
@@ -83,8 +83,8 @@ def test_fused_epilogue(M, N, K, bias, gelu, bf16, pad):
     ba, bw = 4, 4 if M < 1000 else 3
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K + 7)
     cba, cbw = oq.lloydmax_codebook(ba, K), oq.lloydmax_codebook(bw, K)
-    xp = torch.from_numpy(oracle.pack_codes(xc.numpy(), ba)).to(DEV)
-    wp = torch.from_numpy(oracle.pack_codes(wc.numpy(), bw)).to(DEV)
+    xp = torch.from_numpy(oracle.pack_codes(oracle.to_labels(xc.numpy(), ba), ba)).to(DEV)
+    wp = torch.from_numpy(oracle.pack_codes(oracle.to_labels(wc.numpy(), bw), bw)).to(DEV)
     g = torch.Generator()
     g.manual_seed(N)
     b = torch.randn(N, generator=g).to(torch.bfloat16) if bias else None
@@ -148,9 +148,11 @@ def test_c4_up_shape_sampled_rows():
     wc = torch.randint(0, 16, (N, K), generator=g, device=DEV, dtype=torch.int64)
     xs = workloads.random_norms(M, 4, 0, device=DEV)
     wr = workloads.random_norms(N, 4, 1, device=DEV).to(torch.bfloat16)
-    # pack on the device with plain torch ops (LSB-first nibbles), outside the HIP path
-    xp = (xc[:, 0::2] | (xc[:, 1::2] << 4)).to(torch.uint8)
-    wp = (wc[:, 0::2] | (wc[:, 1::2] << 4)).to(torch.uint8)
+    # store on the device with plain torch ops (sign-magnitude labels of the level indices in
+    # LSB-first nibbles), outside the HIP path
+    xl, wl = (torch.where(c >= 8, c - 8, 15 - c) for c in (xc, wc))
+    xp = (xl[:, 0::2] | (xl[:, 1::2] << 4)).to(torch.uint8)
+    wp = (wl[:, 0::2] | (wl[:, 1::2] << 4)).to(torch.uint8)
     cb = oq.lloydmax_codebook(4, K)
     Y = oq.orbit_qlinear(cb, xp, xs, cb, wp, wr)
     torch.cuda.synchronize()

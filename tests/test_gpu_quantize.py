@@ -149,9 +149,12 @@ def test_zero_rows(bits):
     X[2] = 0
     X[7] = 0
     codes, norms = quantize_gpu(X, bits)
-    gc = oracle.unpack_codes(codes.cpu().numpy(), bits, 256)
+    labels = oracle.unpack_codes(codes.cpu().numpy(), bits, 256)
+    gc = oracle.from_labels(labels, bits)
     assert norms[2].item() == 0.0 and norms[7].item() == 0.0
+    # u = 0 sits on the middle threshold: the upper level, index 2^(b-1), stored as label 0
     assert np.all(gc[2] == 1 << (bits - 1)) and np.all(gc[7] == 1 << (bits - 1))
+    assert np.all(labels[2] == 0) and np.all(labels[7] == 0)
     cw, nw = quantize_gpu(X, bits, weights=True)
     assert nw[2].item() == 0.0
 
@@ -271,12 +274,15 @@ def test_sign_symmetry(bits):
     X = _randn_bf16(65, 3072, seed=21)
     c_pos, n_pos = quantize_gpu(X, bits)
     c_neg, n_neg = quantize_gpu(-X, bits)
-    gp = oracle.unpack_codes(c_pos.cpu().numpy(), bits, 3072)
-    gn = oracle.unpack_codes(c_neg.cpu().numpy(), bits, 3072)
+    lp = oracle.unpack_codes(c_pos.cpu().numpy(), bits, 3072)
+    ln = oracle.unpack_codes(c_neg.cpu().numpy(), bits, 3072)
+    gp, gn = oracle.from_labels(lp, bits), oracle.from_labels(ln, bits)
     ocb = oracle.lloydmax_codebook(bits, 3072)
     _, _, U = oracle.quantize_act(to_f64(X), oracle.rpbh_plan(3072, 128, 0), ocb)
     near = oracle.near_tie_mask(U, ocb.thresholds, 1e-5)
     bad = int(np.sum((gn != (1 << bits) - 1 - gp) & ~near))
+    # in the stored labels the mirror flips the sign bit only
+    bad += int(np.sum((ln != (lp ^ (1 << (bits - 1)))) & ~near))
     log_stats(f"sign symmetry b={bits}", near_ties=int(near.sum()), mismatches_off_tie=bad)
     assert bad == 0
     assert torch.equal(n_pos, n_neg)

@@ -65,6 +65,31 @@ def test_pack_hand_computed_bytes():
     assert p6.tolist() == [[0xC5, 0x0F, 0x84]]
 
 
+def test_labels_hand_computed():
+    # b=4: index 0 (most negative) -> 15, 7 -> 8, 8 (smallest positive) -> 0, 15 -> 7
+    assert oracle.to_labels(np.array([0, 7, 8, 15]), 4).tolist() == [15, 8, 0, 7]
+    # b=2: indices 0..3 (levels -a, -b, +b, +a with a > b) -> 3, 2, 0, 1
+    assert oracle.to_labels(np.arange(4), 2).tolist() == [3, 2, 0, 1]
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4, 6])
+def test_labels_are_sign_and_magnitude_rank(bits):
+    # the stored label: top bit = sign of the level, low bits = rank of |level| within its sign
+    levels = oracle.lloydmax_codebook(bits, 3072).levels
+    half = 1 << (bits - 1)
+    idx = np.arange(2 * half)
+    lab = oracle.to_labels(idx, bits)
+    assert sorted(lab.tolist()) == idx.tolist()                  # a bijection
+    assert np.array_equal(oracle.from_labels(lab, bits), idx)    # and from_labels inverts it
+    assert np.array_equal(lab >= half, levels < 0)
+    for neg in (False, True):
+        sel = (levels < 0) == neg
+        mags = np.abs(levels[sel])[np.argsort(lab[sel] & (half - 1))]
+        assert np.all(np.diff(mags) > 0)                         # rank 0 is nearest zero
+    # the antisymmetric partner of a level differs only in the sign bit
+    assert np.array_equal(oracle.to_labels(2 * half - 1 - idx, bits), lab ^ half)
+
+
 @pytest.mark.parametrize("bits", [2, 3, 4, 6])
 def test_pack_roundtrip(bits):
     rng = np.random.default_rng(bits)

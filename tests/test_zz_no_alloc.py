@@ -25,8 +25,8 @@ def _operands(M, N, K, ba, bw, seed):
     xs = workloads.random_norms(M, seed, 0)
     wr = workloads.random_norms(N, seed, 1).to(torch.bfloat16)
     cba, cbw = oq.lloydmax_codebook(ba, K), oq.lloydmax_codebook(bw, K)
-    dev = (torch.from_numpy(oracle.pack_codes(xc.numpy(), ba)).to(DEV), xs.to(DEV),
-           torch.from_numpy(oracle.pack_codes(wc.numpy(), bw)).to(DEV), wr.to(DEV))
+    dev = (torch.from_numpy(oracle.pack_codes(oracle.to_labels(xc.numpy(), ba), ba)).to(DEV), xs.to(DEV),
+           torch.from_numpy(oracle.pack_codes(oracle.to_labels(wc.numpy(), bw), bw)).to(DEV), wr.to(DEV))
     return (xc, xs, wc, wr), (cba, cbw), dev
 
 
