@@ -238,14 +238,14 @@ def main():
         "call_ms_in_step": [float(v) for v in gemm_ms],
         "workspace_bytes": [oq.orbit_qlinear_workspace_size(L["lin"].M, L["lin"].N, L["lin"].K) for L in layers],
     }
-    # The quantizer's launches timed alone as well (back to back, each bracketed by its own events);
-    # inside the step each one follows a GEMM, whose power draw holds the clock down for a while.
+    # The quantizer's launches timed alone as well (back to back between one event pair); inside the
+    # step each one follows a GEMM, whose power draw holds the clock down for a while.
     # Rows of K = 1024 .. 16384 (a multiple of 128 and of h) with h = 128 .. 1024 run the
     # one-row-per-workgroup kernel; its last template argument is log2(h / 128).
     q_alone = []
     for L in layers:
         fn = (lambda L=L: oq.rpbh_quantize_act(L["plan"], L["cba"], L["X"], 1e-10, L["xc"], L["xn"]))
-        q_alone.append(_timed(fn, args.part_reps)[0])
+        q_alone.append(_timed_back_to_back(fn, args.part_reps))
     qkern = [(f"rpbh_quantize_row_kernel<{L['lin'].ba}, false, {L['lin'].h.bit_length() - 8}>"
               if 128 <= L["lin"].h <= 1024 and L["lin"].K % 128 == 0 and L["lin"].K % L["lin"].h == 0
               and 1024 <= L["lin"].K <= 16384 else
@@ -260,8 +260,9 @@ def main():
         "unit": "GB/s",
         "frac": qa_gbs / HBM_PEAK_GBS,
         "traffic": (traffic or {}).get("quant_bytes_per_launch"),
-        "achieved_is": "algorithmic bytes of the step's quantizer launches / their HIP-event times, each launch "
-                       "timed alone (back to back); 'in_step' gives the same launches inside the step",
+        "achieved_is": "algorithmic bytes of the step's quantizer launches / their average HIP-event time, each "
+                       "layer's launch repeated back to back between one event pair; 'in_step' gives the same "
+                       "launches inside the step",
         "launches": [{"linear": L["lin"].name, "M": L["lin"].M, "K": L["lin"].K, "bits": L["lin"].ba,
                       "ms": q_alone[i], "algorithmic_bytes": float(qbytes[i]),
                       "gbs": float(qbytes[i]) / (q_alone[i] * 1e-3) / 1e9,
@@ -274,6 +275,10 @@ def main():
     paper_h = rot = fused = chain = a6 = None
     if args.extras:
         paper_h, rot, fused, chain, a6 = extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms)
+        # the rule's rate against the same layer's h = 128 launch, both timed back to back
+        for i, L in enumerate(layers):
+            e = paper_h[L["lin"].name]
+            e["rate_vs_h128"] = q_alone[i] / e["ms"]
 
     configs = None
     if args.config_reps > 0:
@@ -527,6 +532,22 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     return paper_h, rot, fused, chain, a6
 
 
+def _timed_back_to_back(fn, reps):
+    """Average time of one of `reps` launches of fn issued back to back between one pair of HIP
+    events on the current stream (after one untimed launch): the rate of a kernel run in a
+    sequence, without an event pair around every launch (which adds several microseconds to a
+    0.1 ms launch)."""
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
 def _timed(fn, reps, before=None):
     """Mean, median and minimum of `reps` launches of fn, each bracketed by its own HIP events on the
     current stream; `before` (untimed) runs ahead of each launch."""
@@ -664,13 +685,13 @@ def rotation_per_image(oq, dev, reps):
             _, signs = pr.arrays()
             pb = oq.rpbh_plan_from_arrays(d, pr.h, np.arange(d), signs)
             for name, plan in (("rpbh", pr), ("block_rht", pb)):
-                ms = _timed(lambda: oq.rpbh_quantize_act(plan, cb, X, 1e-10, xc, xn), reps)[0]
+                ms = _timed_back_to_back(lambda: oq.rpbh_quantize_act(plan, cb, X, 1e-10, xc, xn), reps)
                 row[f"{name}_{tag}_ms"] = ms
                 row[f"{name}_{tag}_h"] = pr.h
                 tot[f"{name}_{tag}"] += ms * count * FLUX_STEPS
         Q = (torch.randn((d, d), generator=g, device=dev) / d ** 0.5).to(torch.bfloat16)
         Xr = torch.empty((M, d), dtype=torch.bfloat16, device=dev)
-        ms = _timed(lambda: torch.matmul(X, Q, out=Xr), max(3, reps // 2))[0]
+        ms = _timed_back_to_back(lambda: torch.matmul(X, Q, out=Xr), max(3, reps // 2))
         row["dense_haar_ms"] = ms
         tot["dense_haar"] += ms * count * FLUX_STEPS
         per_shape.append(row)
