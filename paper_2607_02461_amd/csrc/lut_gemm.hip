@@ -354,7 +354,7 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
 // of a block tile is decoded once per K-step into a double-buffered bf16 tile in LDS (147 KB),
 // which halves the decodes per flop of the 128x128 kernel.  While the matrix cores work on step
 // s, each wave decodes step s+1 into the other stage, a quarter per 16-wide k slice, and the
-// codes of step s+2 are in flight.  Block tiles are visited so that the
+// codes of steps s+2 and s+3 are in flight.  Block tiles are visited so that the
 // workgroups resident on one XCD (round-robin dispatch) share A and B panels in that XCD's L2.
 constexpr int BM2 = 256, BN2 = 256, BK2 = 64;
 constexpr int LDS2_STRIDE = BK2 + 8;                  // halves per tile row; 144 B keeps 16-byte
@@ -409,8 +409,8 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     const __bf16* const b_frag0 = lds + LDS2_TILE + (wn * 64 + (lane & 31)) * LDS2_STRIDE + (lane >> 5) * 8;
     constexpr int STAGE = 2 * LDS2_TILE;
 
-    Codes<BA> wa, xa;
-    Codes<BW> wb, xb;
+    Codes<BA> wa, xa, ya;
+    Codes<BW> wb, xb, yb;
     load_codes32<BA>(asrc, wa);
     load_codes32<BW>(bsrc, wb);
 #pragma unroll
@@ -422,9 +422,11 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
         *(uint4*)(a_dst0 + LDS2_TILE + 8 * g) = make_uint4(db[0], db[1], db[2], db[3]);
     }
     {
-        const int64_t s1 = nk > 1 ? 1 : 0;
+        const int64_t s1 = nk > 1 ? 1 : 0, s2 = nk > 2 ? 2 : nk - 1;
         load_codes32<BA>(asrc + s1 * astep, wa);
         load_codes32<BW>(bsrc + s1 * bstep, wb);
+        load_codes32<BA>(asrc + s2 * astep, ya);
+        load_codes32<BW>(bsrc + s2 * bstep, yb);
     }
     __syncthreads();
 
@@ -448,12 +450,12 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     // One K-step in four 16-wide slices.  Slices 0-2 decode the codes of step s+1 (ca, cb) into
     // the other stage while their MFMAs run; then one barrier makes that stage complete and
     // retires every read of this step's stage, so slice 3 can already fetch the next step's
-    // first fragments while its MFMAs run.  The codes of step s+2 load into (na, nb).  The loop
-    // below is unrolled by two so that the code registers swap roles instead of being copied (a
-    // copy would wait for the load).
+    // first fragments while its MFMAs run.  The codes of step s+3 load into (na, nb), so each
+    // load has two K-steps to land.  Three register sets rotate: the loop below is unrolled by
+    // three so that they change roles instead of being copied (a copy would wait for the load).
     auto kstep = [&](int s, const Codes<BA>& ca, const Codes<BW>& cb, Codes<BA>& na, Codes<BW>& nb) {
         // the last steps re-load the final step's codes; they are never used
-        const int64_t s2 = min(s + 2, nk - 1);
+        const int64_t s2 = min(s + 3, nk - 1);
         load_codes32<BA>(asrc + s2 * astep, na);
         load_codes32<BW>(bsrc + s2 * bstep, nb);
         __builtin_amdgcn_sched_barrier(0);
@@ -502,11 +504,13 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
     };
 
     int s = 0;
-    for (; s + 1 < nk; s += 2) {
+    for (; s + 2 < nk; s += 3) {
         kstep(s, wa, wb, xa, xb);
-        kstep(s + 1, xa, xb, wa, wb);
+        kstep(s + 1, ya, yb, wa, wb);
+        kstep(s + 2, xa, xb, ya, yb);
     }
     if (s < nk) kstep(s, wa, wb, xa, xb);
+    if (s + 1 < nk) kstep(s + 1, ya, yb, wa, wb);
 
     // epilogue.  The MFMAs computed the transposed tile, so element e of accumulator (i, j)
     // belongs to row i*32 + lane%32 and column j*32 + 8*(e/4) + 4*(lane/32) + e%4: each lane

@@ -60,8 +60,10 @@ def test_random_codes(M, N, K, ba, bw):
 # that is mostly empty, so the large kernel takes the rows of its full rounds and the 128x128
 # kernel the rest (shifted operands and output, ragged in M and N); 3900 x 8000 fills exactly two
 # rounds (16 x 32 tiles) and runs the large kernel alone, ragged in both.
-@pytest.mark.parametrize("M,N,K", [(4133, 8061, 64), (4133, 8061, 192), (8197, 4099, 1024), (4133, 4099, 320),
-                                   (3900, 8000, 192)])
+# K-step counts 1, 2, 3, 4, 5, 16 cover the large kernel's three-set code ring: no full round, whole
+# rounds, and each length of the remainder
+@pytest.mark.parametrize("M,N,K", [(4133, 8061, 64), (4133, 8061, 128), (4133, 8061, 192), (4133, 8061, 256),
+                                   (8197, 4099, 1024), (4133, 4099, 320), (3900, 8000, 192)])
 @pytest.mark.parametrize("ba,bw", [(4, 4), (4, 3), (2, 2), (3, 4), (6, 4), (6, 2)])
 def test_random_codes_large_tiles(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)
