@@ -221,11 +221,21 @@ __device__ __forceinline__ void store_one(const GemmParams& p, int64_t row, int6
 
 // SPLIT: workgroup z of a K-split contracts K-steps z*steps .. (z+1)*steps - 1 (the last split
 // fewer) and stores its raw sums to p.ws[z][M][N]; lut_gemm_reduce applies the epilogue.
+//
+// 128x128 block tiles, K-step 64, four waves of 64x64.  This kernel serves grids too small for the
+// 256x256 kernel (often one workgroup per compute unit, so one wave per SIMD), where each
+// workgroup's time is its chain of K-steps: it is pipelined like the large kernel.  The block
+// tile's codes are decoded once per K-step into a double-buffered bf16 tile in LDS (74 KB); while
+// the matrix cores work on step s, each wave decodes step s+1 into the other stage (groups 0-1,
+// 2, 3 in slices 0, 1, 2), fragments are read one 16-wide slice ahead, one barrier per step sits
+// before the last slice, and the codes of the next five steps are in flight.
+constexpr int SMALL_TILE = BM * LDS_STRIDE;  // halves per operand tile
+
 template <int BA, int BW, bool SPLIT>
 __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
-    __shared__ __align__(16) __bf16 As[BM * LDS_STRIDE];
-    __shared__ __align__(16) __bf16 Bs[BN * LDS_STRIDE];
-    __shared__ uint32_t tab6[BA == 6 ? 64 : 1];  // 6-bit activation levels (bf16 in the low half)
+    extern __shared__ __align__(16) __bf16 slds[];  // [stage][A, B][128][72], then the 6-bit table
+    constexpr int STAGE = 2 * SMALL_TILE;
+    uint32_t* const tab6 = (uint32_t*)(slds + 2 * STAGE);  // 6-bit activation levels (bf16 in the low half)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
@@ -254,98 +264,205 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    // The codes of the next D K-steps are in flight while a step is decoded and contracted: on
-    // small grids each workgroup's time is its chain of K-steps, which would otherwise wait for
-    // one global load per step.  The ring is unrolled so that every slot is a fixed register set.
-    constexpr int D = 4;  // the ring's slots (unrolled below)
     const int64_t astep = BK * BA / 8, bstep = BK * BW / 8;
-    Codes<BA> ca[D];
-    Codes<BW> cb[D];
+    __bf16* const a_dst0 = slds + lr * LDS_STRIDE + lh * 32;  // this thread's decode slots, stage 0
+    const __bf16* const a_frag0 = slds + (wm * 64 + (lane & 31)) * LDS_STRIDE + (lane >> 5) * 8;
+    const __bf16* const b_frag0 = slds + SMALL_TILE + (wn * 64 + (lane & 31)) * LDS_STRIDE + (lane >> 5) * 8;
+
+    auto decode_group = [&](int stage, int g, const Codes<BA>& ca, const Codes<BW>& cb) {
+        uint32_t da[4], db[4];
+        decode8<BA>(ca, g, ta, tab6, da);
+        decode8<BW>(cb, g, tw, nullptr, db);
+        *(uint4*)(a_dst0 + stage + 8 * g) = make_uint4(da[0], da[1], da[2], da[3]);
+        *(uint4*)(a_dst0 + stage + SMALL_TILE + 8 * g) = make_uint4(db[0], db[1], db[2], db[3]);
+    };
+
+    // a ring of RING code register sets: set u holds the codes of the steps congruent to u, so
+    // each load has RING - 1 K-steps to land (a workgroup here is often alone on its compute unit,
+    // with nothing else to cover the memory latency)
+    constexpr int RING = 6;
+    Codes<BA> ca[RING];
+    Codes<BW> cb[RING];
+    load_codes32<BA>(asrc, ca[0]);
+    load_codes32<BW>(bsrc, cb[0]);
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-        const int64_t s = min(d, nk - 1);
-        load_codes32<BA>(asrc + s * astep, ca[d]);
-        load_codes32<BW>(bsrc + s * bstep, cb[d]);
+    for (int g = 0; g < 4; ++g) decode_group(0, g, ca[0], cb[0]);
+#pragma unroll
+    for (int u = 1; u < RING; ++u) {
+        const int64_t su = min(u, nk - 1);
+        load_codes32<BA>(asrc + su * astep, ca[u]);
+        load_codes32<BW>(bsrc + su * bstep, cb[u]);
     }
-    uint4* const adst = (uint4*)(As + lr * LDS_STRIDE + lh * 32);
-    uint4* const bdst = (uint4*)(Bs + lr * LDS_STRIDE + lh * 32);
-    auto step = [&](int s, Codes<BA>& wa, Codes<BW>& wb) {
+    __syncthreads();
+
+    // fragments of one 16-wide k slice of a stage
+    bf16x8 a[2][2], b[2][2];
+    auto read_frags = [&](int stage, int kk, bf16x8 (&af)[2], bf16x8 (&bf)[2]) {
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            uint32_t da[4], db[4];
-            decode8<BA>(wa, g, ta, tab6, da);
-            decode8<BW>(wb, g, tw, nullptr, db);
-            adst[g] = make_uint4(da[0], da[1], da[2], da[3]);
-            bdst[g] = make_uint4(db[0], db[1], db[2], db[3]);
-        }
-        {
-            // this slot's next codes (the last steps re-load the final step's, never used)
-            const int64_t sn = min(s + D, nk - 1);
-            load_codes32<BA>(asrc + sn * astep, wa);
-            load_codes32<BW>(bsrc + sn * bstep, wb);
-        }
-        __syncthreads();
+        for (int i = 0; i < 2; ++i) af[i] = *(const bf16x8*)(a_frag0 + stage + i * 32 * LDS_STRIDE + kk * 16);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) bf[j] = *(const bf16x8*)(b_frag0 + stage + j * 32 * LDS_STRIDE + kk * 16);
+    };
+    read_frags(0, 0, a[0], b[0]);
+
+    // as the large kernel's K-step: decode step s+1 (codes ca, cb) in slices 0-2, barrier before
+    // slice 3, whose MFMAs overlap the next step's first fragments; the codes of step s+RING load
+    // into (na, nb), the set step s came from
+    auto kstep = [&](int s, const Codes<BA>& ca, const Codes<BW>& cb, Codes<BA>& na, Codes<BW>& nb) {
+        // the last steps re-load the final step's codes; they are never used
+        const int64_t sl = min(s + RING, nk - 1);
+        load_codes32<BA>(asrc + sl * astep, na);
+        load_codes32<BW>(bsrc + sl * bstep, nb);
+        __builtin_amdgcn_sched_barrier(0);
+
+        const int cur = (s & 1) * STAGE, nxt = STAGE - cur;
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
-            bf16x8 a[2], b[2];
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-                a[i] = *(const bf16x8*)(As + (wm * 64 + i * 32 + (lane & 31)) * LDS_STRIDE + kk * 16 + (lane >> 5) * 8);
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                b[j] = *(const bf16x8*)(Bs + (wn * 64 + j * 32 + (lane & 31)) * LDS_STRIDE + kk * 16 + (lane >> 5) * 8);
+            const int f = kk & 1;
+            if (kk == 3) __syncthreads();
+            if (kk < 3) read_frags(cur, kk + 1, a[f ^ 1], b[f ^ 1]);
+            else read_frags(nxt, 0, a[f ^ 1], b[f ^ 1]);
+            if (kk == 0) {
+                decode_group(nxt, 0, ca, cb);
+                decode_group(nxt, 1, ca, cb);
+            } else if (kk < 3) {
+                decode_group(nxt, kk + 1, ca, cb);
+            }
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[f][j], a[f][i], acc[i][j], 0, 0, 0);
+            // next fragments first, then each MFMA followed by a share of the decode, the decoded
+            // rows' LDS writes last
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+            if (kk == 0) {
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 15, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 4, 0);
+            } else if (kk < 3) {
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
-        __syncthreads();
     };
-    // whole rounds of the ring without branches (so each decode waits only for its own slot's
-    // load), then the 0-3 remaining steps
-    int s = 0;
-    for (; s + D <= nk; s += D) {
-        step(s, ca[0], cb[0]);
-        step(s + 1, ca[1], cb[1]);
-        step(s + 2, ca[2], cb[2]);
-        step(s + 3, ca[3], cb[3]);
-    }
-    if (s < nk) step(s, ca[0], cb[0]);
-    if (s + 1 < nk) step(s + 1, ca[1], cb[1]);
-    if (s + 2 < nk) step(s + 2, ca[2], cb[2]);
 
-    // epilogue: acc element e of a 32x32 tile sits at row 8*(e/4) + 4*(lane/32) + e%4, col lane%32
+    // step s + u decodes set (u + 1) % RING and refills set u; unrolled by RING so that every set
+    // index is a constant (registers, none copied)
+    int s = 0;
+    for (; s + RING - 1 < nk; s += RING) {
+#pragma unroll
+        for (int u = 0; u < RING; ++u) kstep(s + u, ca[(u + 1) % RING], cb[(u + 1) % RING], ca[u], cb[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < RING - 1; ++u)
+        if (s + u < nk) kstep(s + u, ca[(u + 1) % RING], cb[(u + 1) % RING], ca[u], cb[u]);
+
+    // epilogue.  As in the large kernel, the MFMAs computed the transposed tile: element e of
+    // accumulator (i, j) belongs to row i*32 + lane%32 and column j*32 + 8*(e/4) + 4*(lane/32) + e%4,
+    // so each lane holds runs of four consecutive columns of one row and stores each run as one
+    // vector.  Every load comes before the first store (as far as the compiler knows, Y may alias
+    // xn, wn or the bias, and a wait placed among the stores would make each store wait for the
+    // one before).
+    const int64_t col0 = n0 + wn * 64 + 4 * (lane >> 5);
     if constexpr (SPLIT) {
         float* const ws = p.ws + (int64_t)blockIdx.z * p.M * p.N;
+        const bool vec = (p.N & 3) == 0;
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 2; ++i) {
+            const int64_t row = m0 + wm * 64 + i * 32 + (lane & 31);
+            if (row >= p.M) continue;
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
-                if (col >= p.N) continue;
+            for (int j = 0; j < 2; ++j)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int64_t row = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                    if (row < p.M) ws[row * p.N + col] = acc[i][j][e];
+                for (int q = 0; q < 4; ++q) {
+                    const int64_t c = col0 + j * 32 + 8 * q;
+                    float* const dst = ws + row * p.N + c;
+                    if (vec && c + 3 < p.N) {
+                        *(float4*)dst = make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                                    acc[i][j][4 * q + 3]);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (c + r < p.N) dst[r] = acc[i][j][4 * q + r];
+                    }
                 }
-            }
+        }
         return;
     }
+    float xsv[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
+        const int64_t row = m0 + wm * 64 + i * 32 + (lane & 31);
+        xsv[i] = row < p.M ? p.xn[row] : 0.f;
+    }
+    uint2 rwv[2][4], bv[2][4];  // bf16 r' and bias of the lane's columns, four per (j, run)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
-            if (col >= p.N) continue;
-            const float rw = bf16_to_f32(p.wn[col]);
-            const float bias = p.bias ? bf16_to_f32(p.bias[col]) : 0.f;
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int64_t row = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-                if (row < p.M) store_one(p, row, col, epilogue_value(p, acc[i][j][e] * p.xn[row] * rw, bias));
+        for (int q = 0; q < 4; ++q) {
+            const int64_t c = col0 + j * 32 + 8 * q;
+            if (c + 3 < p.N && p.vec4) {
+                rwv[j][q] = *(const uint2*)(p.wn + c);
+                bv[j][q] = p.bias ? *(const uint2*)(p.bias + c) : make_uint2(0u, 0u);
+            } else {
+                uint16_t v[4], w[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    v[r] = c + r < p.N ? p.wn[c + r] : (uint16_t)0;
+                    w[r] = p.bias && c + r < p.N ? p.bias[c + r] : (uint16_t)0;
+                }
+                rwv[j][q] = make_uint2(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16));
+                bv[j][q] = make_uint2(w[0] | ((uint32_t)w[1] << 16), w[2] | ((uint32_t)w[3] << 16));
             }
         }
+    // every output value first, then the stores
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint2 rw = rwv[j][q], bb = bv[j][q];
+                const float r4[4] = {__uint_as_float(rw.x << 16), __uint_as_float(rw.x & 0xFFFF0000u),
+                                     __uint_as_float(rw.y << 16), __uint_as_float(rw.y & 0xFFFF0000u)};
+                const float b4[4] = {__uint_as_float(bb.x << 16), __uint_as_float(bb.x & 0xFFFF0000u),
+                                     __uint_as_float(bb.y << 16), __uint_as_float(bb.y & 0xFFFF0000u)};
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    acc[i][j][4 * q + r] = epilogue_value(p, acc[i][j][4 * q + r] * xsv[i] * r4[r], b4[r]);
+            }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int64_t row = m0 + wm * 64 + i * 32 + (lane & 31);
+        if (row >= p.M) continue;
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int64_t c = col0 + j * 32 + 8 * q;
+                const float v[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                const bool full = c + 3 < p.N && p.vec4;
+                if (full && p.out_bf16) {
+                    *(uint2*)((uint16_t*)p.Y + row * p.ldy + c) =
+                        make_uint2(f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16),
+                                   f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16));
+                } else if (full) {
+                    *(float4*)((float*)p.Y + row * p.ldy + c) = make_float4(v[0], v[1], v[2], v[3]);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (c + r < p.N) store_one(p, row, c + r, v[r]);
+                }
+            }
     }
 }
 
@@ -549,11 +666,19 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
                 bv[j][q] = make_uint2(v[0] | ((uint32_t)v[1] << 16), v[2] | ((uint32_t)v[3] << 16));
             }
         }
+    // the lane's four row norms before the first store (Y may alias xn as far as the compiler
+    // knows, so a load after a store would wait for it)
+    float xsv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t row = m0 + wm * 128 + i * 32 + (lane & 31);
+        xsv[i] = row < p.M ? p.xn[row] : 0.f;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int64_t row = m0 + wm * 128 + i * 32 + (lane & 31);
         if (row >= p.M) continue;
-        const float xs = p.xn[row];
+        const float xs = xsv[i];
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
 #pragma unroll
@@ -660,16 +785,22 @@ __global__ __launch_bounds__(256) void lut_gemm_reduce(GemmParams p, int splits)
 template <int BA, int BW>
 hipError_t launch_small(const GemmParams& p, hipStream_t stream) {
     dim3 grid((unsigned)((p.N + BN - 1) / BN), (unsigned)((p.M + BM - 1) / BM));
+    const size_t smem = (size_t)2 * 2 * SMALL_TILE * sizeof(__bf16) + (BA == 6 ? 64 * sizeof(uint32_t) : 0);
+    static std::atomic<uint64_t> attr_split{0}, attr_whole{0};
     if (p.ws && p.splits > 1) {
+        const hipError_t ea = raise_lds_limit((const void*)lut_gemm_kernel<BA, BW, true>, (int)smem, attr_split);
+        if (ea != hipSuccess) return ea;
         grid.z = (unsigned)p.splits;
-        hipLaunchKernelGGL((lut_gemm_kernel<BA, BW, true>), grid, dim3(256), 0, stream, p);
+        hipLaunchKernelGGL((lut_gemm_kernel<BA, BW, true>), grid, dim3(256), smem, stream, p);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int64_t threads = p.M * ((p.N + 3) / 4);
         hipLaunchKernelGGL(lut_gemm_reduce, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, p, p.splits);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((lut_gemm_kernel<BA, BW, false>), grid, dim3(256), 0, stream, p);
+    const hipError_t ew = raise_lds_limit((const void*)lut_gemm_kernel<BA, BW, false>, (int)smem, attr_whole);
+    if (ew != hipSuccess) return ew;
+    hipLaunchKernelGGL((lut_gemm_kernel<BA, BW, false>), grid, dim3(256), smem, stream, p);
     return hipGetLastError();
 }
 
