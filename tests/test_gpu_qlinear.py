@@ -42,10 +42,11 @@ def _gpu(xc, xs, wc, wr, ba, bw, K):
     return Y.cpu().numpy().astype(np.float64)
 
 
-# the 128 x 128 kernel keeps the codes of 4 K-steps in flight: step counts 1, 2, 4, 5, 7, 8, 48, 216
-# cover full rounds of that ring and each length of the remainder
+# the 128 x 128 kernel keeps the codes of 5 K-steps in flight in 6 register sets: step counts 1, 2,
+# 3, 4, 5, 7, 8, 9, 48, 216 cover no full round of that ring, whole rounds and each remainder
 @pytest.mark.parametrize("M,N,K", [(1, 128, 64), (257, 384, 256), (300, 130, 512), (64, 3072, 3072),
-                                   (129, 257, 13824), (5, 1, 128), (70, 96, 320), (33, 200, 448)])
+                                   (129, 257, 13824), (5, 1, 128), (70, 96, 320), (33, 200, 448),
+                                   (40, 200, 192), (40, 200, 576)])
 @pytest.mark.parametrize("ba,bw", [(4, 4), (4, 3), (4, 2), (3, 3), (2, 2), (3, 4), (2, 4), (6, 4), (6, 3), (6, 2)])
 def test_random_codes(M, N, K, ba, bw):
     xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + N + K)

@@ -48,8 +48,8 @@ def _splits(M, N, K, n):
 
 
 # Ragged M and N, one token, c1's layer (256 x 3072 x 3072).  On 256 compute units the split
-# lengths (K-steps per split, then the last split's) cover each remainder of the kernel's 4-slot
-# ring: 5/4, 10/8, 6/6, 5/3, 4/4, 8/1, 7/1, 5/2 and 6/3.
+# lengths (K-steps per split, then the last split's: 5/4, 10/8, 6/6, 5/3, 4/4, 8/1, 7/1, 5/2 and
+# 6/3) cover each remainder of the kernel's 6-set code ring, with and without a full round.
 @pytest.mark.parametrize("M,N,K", [(300, 130, 1216), (256, 3072, 3072), (129, 257, 13824), (1, 3072, 3072),
                                    (64, 1000, 4096), (200, 1000, 7232), (200, 1000, 6336), (1, 96, 1088),
                                    (200, 1000, 5184)])
