@@ -279,6 +279,10 @@ def main():
         for i, L in enumerate(layers):
             e = paper_h[L["lin"].name]
             e["rate_vs_h128"] = q_alone[i] / e["ms"]
+        # what the vendor library's dense bf16 matmul attains on the same shapes (context for the
+        # GEMM's fraction of the nominal peak)
+        dn = rot["dense_bf16_matmul"]
+        roofline["attainable_dense_bf16_matmul_tflops"] = {L["lin"].name: dn[L["lin"].name]["tflops"] for L in layers}
 
     configs = None
     if args.config_reps > 0:
@@ -431,6 +435,19 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     rot["dense_haar_rotation_gemm_ms"] = e0.elapsed_time(e1) / 5
     rot["shape"] = f"{L0['lin'].M} x {K0}"
     del Qt, Xr
+    # The paper's own layer computation (fake quantization): operands dequantized to BF16 and the
+    # matmul in BF16.  The matmul alone, by the vendor library (hipBLASLt through torch), on each
+    # layer's shape with its bf16 inputs, beside the LUT-decode GEMM's launches on the same shape.
+    dense = {"what": "torch.matmul (hipBLASLt) of the layer's bf16 X and bf16 W^T into bf16, the matmul of the "
+                     "paper's dequantize-then-BF16 path without its dequantization passes"}
+    for L in layers:
+        lin = L["lin"]
+        Wt = L["W"].t().contiguous()
+        Yd = torch.empty((lin.M, lin.N), dtype=torch.bfloat16, device=dev)
+        ms = _timed_back_to_back(lambda: torch.matmul(L["X"], Wt, out=Yd), 5)
+        dense[lin.name] = {"M": lin.M, "K": lin.K, "N": lin.N, "ms": ms,
+                           "tflops": 2.0 * lin.M * lin.N * lin.K / (ms * 1e-3) / 1e12}
+        del Wt, Yd
     # Full RHT (one Hadamard block over the whole row, no permutation) needs a power-of-two d: the
     # first 4096 channels of the same input (a strided view; 2048 of c1's 3072), against RPBH and
     # Block-RHT there
@@ -529,6 +546,7 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
           "gemm_ms": g6_ms, "gemm_tflops": float(flops[0]) / (g6_ms * 1e-3) / 1e12}
     del xc6
 
+    rot["dense_bf16_matmul"] = dense
     return paper_h, rot, fused, chain, a6
 
 
