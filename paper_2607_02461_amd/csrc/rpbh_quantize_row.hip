@@ -12,8 +12,8 @@
 //   gather    16 ds_read_u16 through loop-invariant per-lane byte offsets (the permutation) from
 //             the row staged in LDS; one v_perm pairs two halves per bf16 pair;
 //   stage     the next row streams from HBM straight into the other half of a double-buffered
-//             staging area (global_load_lds_dwordx4, no registers), so one barrier per iteration
-//             suffices;
+//             staging area (global_load_lds_dwordx4, no registers, non-temporal), so one barrier
+//             per iteration suffices;
 //   H_4       the first two butterfly stages of each quad of positions, with the Rademacher signs
 //             of Eq. (9) folded in, as six v_dot2_f32_bf16 (bf16 pairs against per-lane sign pairs
 //             with neg_lo / neg_hi modifiers; the radix-4 form uses the first stage's result as the
@@ -37,6 +37,7 @@ namespace orbit {
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kLaneVals = 16;   // positions per lane
@@ -45,6 +46,8 @@ constexpr int kLaneVals = 16;   // positions per lane
 // 2048 (c / 64) + 1024 b + 16 (c % 64) of the staging area, so the second buffer is the first one
 // 1024 bytes further (an immediate offset of the LDS instructions).
 constexpr int kBufGap = 1024;
+// Cache-policy bits of the staging loads: non-temporal (each row is read once)
+constexpr int kNonTemporal = 2;
 
 // Butterfly between lanes 16 (SPAN = 16) or 32 (SPAN = 32) apart on two registers at once, with
 // v_permlane16_swap / v_permlane32_swap (VALU, no LDS).  The swap trades the upper SPAN lanes of
@@ -242,23 +245,28 @@ __device__ __forceinline__ void pack16(const float (&y)[16], uint32_t (&w)[3]) {
     }
 }
 
-// 2*BITS bytes of packed codes at a 2*BITS-byte aligned offset
+// 2*BITS bytes of packed codes at a 2*BITS-byte aligned offset, stored non-temporal (the codes
+// are written once and not read again by this kernel; the hint keeps them from displacing the
+// streaming rows in the caches)
 template <int BITS>
 __device__ __forceinline__ void store16(uint8_t* dst, const uint32_t (&w)[3]) {
     if constexpr (BITS == 4) {
-        *(uint2*)dst = make_uint2(w[0], w[1]);
+        u32x2 v;
+        v.x = w[0];
+        v.y = w[1];
+        __builtin_nontemporal_store(v, (u32x2*)dst);
     } else if constexpr (BITS == 2) {
-        *(uint32_t*)dst = w[0];
+        __builtin_nontemporal_store(w[0], (uint32_t*)dst);
     } else if constexpr (BITS == 6) {
         uint32_t* d = (uint32_t*)dst;
-        d[0] = w[0];
-        d[1] = w[1];
-        d[2] = w[2];
+        __builtin_nontemporal_store(w[0], d);
+        __builtin_nontemporal_store(w[1], d + 1);
+        __builtin_nontemporal_store(w[2], d + 2);
     } else {
         uint16_t* d = (uint16_t*)dst;   // 6 bytes at an even offset
-        d[0] = (uint16_t)w[0];
-        d[1] = (uint16_t)(w[0] >> 16);
-        d[2] = (uint16_t)w[1];
+        __builtin_nontemporal_store((uint16_t)w[0], d);
+        __builtin_nontemporal_store((uint16_t)(w[0] >> 16), d + 1);
+        __builtin_nontemporal_store((uint16_t)w[1], d + 2);
     }
 }
 
@@ -271,7 +279,6 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
     const int blk = tid >> 3, q = tid & 7;
     const int nb = p.nb;
     float* const part = (float*)(smem + p.part_off);
-    unsigned char* const stage = smem + p.row_off;
 
     // Stages across lanes.  An h-block (h = 128 * 2^OUTER) spans L = h/16 consecutive, aligned lanes
     // and its Hadamard stages pair lane j with j ^ v along a basis of the lane-index bits:
@@ -345,7 +352,7 @@ __global__ __launch_bounds__(1024) void rpbh_quantize_row_kernel(QuantParams p) 
             __attribute__((address_space(3))) void* dst = (__attribute__((address_space(3))) void*)(
                 (__attribute__((address_space(3))) unsigned char*)smem + p.row_off + 2048u * b + kBufGap * buf);
             if (b < nblk - 1 || lane_in_last)
-                __builtin_amdgcn_global_load_lds((const void*)(base + 1024 * b + lane_off), dst, 16, 0, 0);
+                __builtin_amdgcn_global_load_lds((const void*)(base + 1024 * b + lane_off), dst, 16, 0, kNonTemporal);
         }
     };
 
