@@ -34,7 +34,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=25)
     ap.add_argument("--workload", default="c4_video_mlp_w4a4", choices=["c4_video_mlp_w4a4", "c1_single_w4a4"])
     ap.add_argument("--cpu-baseline-rows", type=int, default=12288,
                     help="token rows of the oracle's timed CPU sample (0 disables it)")
@@ -377,8 +377,7 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     for L in layers:
         lin = L["lin"]
         plan_p = oq.rpbh_plan(lin.K, 0, wl.plan_seed)
-        for _ in range(2):
-            oq.rpbh_quantize_act(plan_p, L["cba"], L["X"], 1e-10, L["xc"], L["xn"])
+        _warm(lambda: oq.rpbh_quantize_act(plan_p, L["cba"], L["X"], 1e-10, L["xc"], L["xn"]))
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(10):
@@ -400,8 +399,7 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     def time_quant(plan_v, reps=10, X=None, cb=None, xc=None, xn=None):
         X = L0["X"] if X is None else X
         cb, xc, xn = (L0["cba"], L0["xc"], L0["xn"]) if cb is None else (cb, xc, xn)
-        for _ in range(2):
-            oq.rpbh_quantize_act(plan_v, cb, X, 1e-10, xc, xn)
+        _warm(lambda: oq.rpbh_quantize_act(plan_v, cb, X, 1e-10, xc, xn))
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(reps):
@@ -424,8 +422,7 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     Qt = Q.t().contiguous().to(torch.bfloat16).to(dev)
     del Q
     Xr = torch.empty((L0["lin"].M, K0), dtype=torch.bfloat16, device=dev)
-    for _ in range(2):
-        torch.matmul(L0["X"], Qt, out=Xr)
+    _warm(lambda: torch.matmul(L0["X"], Qt, out=Xr))
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(5):
@@ -469,9 +466,8 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     # NEXT row: the up-projection with the MLP's GELU and a bf16 output fused into the epilogue
     # (the form that feeds the next quantizer), against the plain fp32 GEMM on the same codes
     Yb = torch.empty((L0["lin"].M, L0["lin"].N), dtype=torch.bfloat16, device=dev)
-    for _ in range(2):
-        oq.orbit_qlinear_ws(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["ws"], gelu=True,
-                            out_dtype=torch.bfloat16, out=Yb)
+    _warm(lambda: oq.orbit_qlinear_ws(L0["cba"], L0["xc"], L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["ws"],
+                                      gelu=True, out_dtype=torch.bfloat16, out=Yb))
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(5):
@@ -507,8 +503,7 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
 
         chain = {"layers": f"{L0['lin'].name} -> GELU -> {L1['lin'].name}"}
         for name, fn in (("fused_ms", chain_fused), ("unfused_ms", chain_unfused)):
-            for _ in range(2):
-                fn()
+            _warm(fn)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
             for _ in range(3):
@@ -524,8 +519,7 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     cb6 = oq.lloydmax_codebook(6, K0)
     xc6 = torch.empty((L0["lin"].M, K0 * 6 // 8), dtype=torch.uint8, device=dev)
     plan0 = L0["plan"]
-    for _ in range(2):
-        oq.rpbh_quantize_act(plan0, cb6, L0["X"], 1e-10, xc6, L0["xn"])
+    _warm(lambda: oq.rpbh_quantize_act(plan0, cb6, L0["X"], 1e-10, xc6, L0["xn"]))
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(10):
@@ -533,8 +527,7 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     e1.record()
     torch.cuda.synchronize()
     q6_ms = e0.elapsed_time(e1) / 10
-    for _ in range(2):
-        oq.orbit_qlinear(cb6, xc6, L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"])
+    _warm(lambda: oq.orbit_qlinear(cb6, xc6, L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"]))
     e0.record()
     for _ in range(5):
         oq.orbit_qlinear(cb6, xc6, L0["xn"], L0["cbw"], L0["wc"], L0["wn"], L0["Y"])
@@ -550,13 +543,33 @@ def extras_entries(oq, workloads, wl, dev, layers, flops, gemm_ms):
     return paper_h, rot, fused, chain, a6
 
 
+# Untimed work ahead of each per-launch measurement.  After an idle spell the GPU's clock takes tens
+# of milliseconds of load to come back: c4-shaped GEMMs issued after 2 s idle ran 18% slower than
+# in steady state over their first ~12 ms and 4% slower over the next 12 ms.
+WARM_MS = 100.0
+
+
+def _warm(fn, before=None, min_ms=WARM_MS):
+    """Untimed launches of fn (each after `before`) until at least min_ms of wall time has passed."""
+    t0 = time.perf_counter()
+    n = 1
+    while True:
+        for _ in range(n):
+            if before is not None:
+                before()
+            fn()
+        torch.cuda.synchronize()
+        if (time.perf_counter() - t0) * 1e3 >= min_ms:
+            return
+        n = min(2 * n, 64)
+
+
 def _timed_back_to_back(fn, reps):
     """Average time of one of `reps` launches of fn issued back to back between one pair of HIP
-    events on the current stream (after one untimed launch): the rate of a kernel run in a
+    events on the current stream (after WARM_MS of untimed launches): the rate of a kernel run in a
     sequence, without an event pair around every launch (which adds several microseconds to a
     0.1 ms launch)."""
-    fn()
-    torch.cuda.synchronize()
+    _warm(fn)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(reps):
@@ -568,10 +581,10 @@ def _timed_back_to_back(fn, reps):
 
 def _timed(fn, reps, before=None):
     """Mean, median and minimum of `reps` launches of fn, each bracketed by its own HIP events on the
-    current stream; `before` (untimed) runs ahead of each launch."""
+    current stream; `before` (untimed) runs ahead of each launch, and WARM_MS of both ahead of the
+    first."""
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-    fn()
-    torch.cuda.synchronize()
+    _warm(fn, before)
     for e0, e1 in ev:
         if before is not None:
             before()
@@ -894,6 +907,7 @@ def adaln_sweep(oq, workloads, dev, steps, warmup=2):
             g.replay()
             torch.cuda.synchronize()
             ok = ok and bool(torch.equal(Y, ref))
+        _warm(g.replay)
         e0.record()
         for _ in range(steps):
             g.replay()
