@@ -674,6 +674,43 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
         const int64_t row = m0 + wm * 128 + i * 32 + (lane & 31);
         xsv[i] = row < p.M ? p.xn[row] : 0.f;
     }
+    // Plain fp32 output with 4-aligned rows: the outputs go through LDS (free after the main loop)
+    // so that each store covers 4 rows of 256 contiguous bytes instead of 32 rows of 32 bytes.
+    // Each wave owns a 64 x 68-float region and turns its 128 x 64 sub-tile around in two halves;
+    // a wave's LDS accesses run in order, so the halves reuse the region without a barrier.
+    if (plain && p.vec4 && (p.N & 3) == 0) {
+        __syncthreads();   // every wave is done reading the stages
+        constexpr int TS = 68;   // region row stride in floats (64 + 4 keeps the accesses conflict-free)
+        float* const tl = (float*)lds + wave * (64 * TS);
+        const int64_t colg = n0 + wn * 64 + 4 * (lane & 15);
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+#pragma unroll
+            for (int ii = 0; ii < 2; ++ii) {
+                const int i = 2 * half + ii;
+                const float xs = xsv[i];
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint2 rw = rwv[j][q];
+                        *(float4*)(tl + (ii * 32 + (lane & 31)) * TS + j * 32 + 8 * q + 4 * (lane >> 5)) =
+                            make_float4(acc[i][j][4 * q + 0] * xs * __uint_as_float(rw.x << 16),
+                                        acc[i][j][4 * q + 1] * xs * __uint_as_float(rw.x & 0xFFFF0000u),
+                                        acc[i][j][4 * q + 2] * xs * __uint_as_float(rw.y << 16),
+                                        acc[i][j][4 * q + 3] * xs * __uint_as_float(rw.y & 0xFFFF0000u));
+                    }
+            }
+#pragma unroll
+            for (int t = 0; t < 16; ++t) {
+                const int r = 4 * t + (lane >> 4);
+                const float4 v = *(const float4*)(tl + r * TS + 4 * (lane & 15));
+                const int64_t row = m0 + wm * 128 + 64 * half + r;
+                if (row < p.M && colg < p.N) *(float4*)((float*)p.Y + row * p.ldy + colg) = v;
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int64_t row = m0 + wm * 128 + i * 32 + (lane & 31);
