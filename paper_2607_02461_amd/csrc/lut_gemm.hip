@@ -373,9 +373,37 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
     // xn, wn or the bias, and a wait placed among the stores would make each store wait for the
     // one before).
     const int64_t col0 = n0 + wn * 64 + 4 * (lane >> 5);
+    // With a multiple of 4 columns (and, for Y, rows that allow 4-wide stores) the outputs go
+    // through LDS, free after the main loop, so that each store covers 4 rows of contiguous bytes
+    // (256 of fp32, 128 of bf16) instead of 32 rows of 16 or 8: each wave writes its 64 x 64
+    // sub-tile into a region of its own (68 floats or 72 bf16 per row, padding that keeps the
+    // accesses conflict-free) and reads it back by rows.
+    constexpr int TS = 68, TSB = 72;
+    float* const tl = (float*)slds + wave * (64 * TS);
+    uint16_t* const tlb = (uint16_t*)tl;
+    const int64_t colg = n0 + wn * 64 + 4 * (lane & 15);
     if constexpr (SPLIT) {
         float* const ws = p.ws + (int64_t)blockIdx.z * p.M * p.N;
         const bool vec = (p.N & 3) == 0;
+        if (vec) {
+            __syncthreads();   // every wave is done reading the stages
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        *(float4*)(tl + (i * 32 + (lane & 31)) * TS + j * 32 + 8 * q + 4 * (lane >> 5)) =
+                            make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+#pragma unroll
+            for (int t = 0; t < 16; ++t) {
+                const int r = 4 * t + (lane >> 4);
+                const int64_t row = m0 + wm * 64 + r;
+                const float4 v = *(const float4*)(tl + r * TS + 4 * (lane & 15));
+                if (row < p.M && colg < p.N) *(float4*)(ws + row * p.N + colg) = v;
+            }
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int64_t row = m0 + wm * 64 + i * 32 + (lane & 31);
@@ -440,6 +468,37 @@ __global__ __launch_bounds__(256) void lut_gemm_kernel(GemmParams p) {
                 for (int r = 0; r < 4; ++r)
                     acc[i][j][4 * q + r] = epilogue_value(p, acc[i][j][4 * q + r] * xsv[i] * r4[r], b4[r]);
             }
+    if (p.vec4 && (p.N & 3) == 0) {
+        __syncthreads();   // every wave is done reading the stages
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int lrow = i * 32 + (lane & 31), lcol = j * 32 + 8 * q + 4 * (lane >> 5);
+                    const float v[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                    if (p.out_bf16)
+                        *(uint2*)(tlb + lrow * TSB + lcol) =
+                            make_uint2(f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16),
+                                       f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16));
+                    else
+                        *(float4*)(tl + lrow * TS + lcol) = make_float4(v[0], v[1], v[2], v[3]);
+                }
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+            const int r = 4 * t + (lane >> 4);
+            const int64_t row = m0 + wm * 64 + r;
+            if (p.out_bf16) {
+                const uint2 v = *(const uint2*)(tlb + r * TSB + 4 * (lane & 15));
+                if (row < p.M && colg < p.N) *(uint2*)((uint16_t*)p.Y + row * p.ldy + colg) = v;
+            } else {
+                const float4 v = *(const float4*)(tl + r * TS + 4 * (lane & 15));
+                if (row < p.M && colg < p.N) *(float4*)((float*)p.Y + row * p.ldy + colg) = v;
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int64_t row = m0 + wm * 64 + i * 32 + (lane & 31);
@@ -674,14 +733,17 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
         const int64_t row = m0 + wm * 128 + i * 32 + (lane & 31);
         xsv[i] = row < p.M ? p.xn[row] : 0.f;
     }
-    // Plain fp32 output with 4-aligned rows: the outputs go through LDS (free after the main loop)
-    // so that each store covers 4 rows of 256 contiguous bytes instead of 32 rows of 32 bytes.
-    // Each wave owns a 64 x 68-float region and turns its 128 x 64 sub-tile around in two halves;
-    // a wave's LDS accesses run in order, so the halves reuse the region without a barrier.
-    if (plain && p.vec4 && (p.N & 3) == 0) {
+    // Rows that allow 4-wide stores (and a multiple of 4 columns): the finished outputs go through
+    // LDS (free after the main loop) so that each store covers 4 rows of contiguous bytes (256 of
+    // fp32, 128 of bf16) instead of 32 rows of 16 or 8 bytes.  Each wave owns a region of 64 rows
+    // (68 floats or 72 bf16 per row, padding that keeps the accesses conflict-free) and turns its
+    // 128 x 64 sub-tile around in two halves; a wave's LDS accesses run in order, so the halves
+    // reuse the region without a barrier.
+    if (p.vec4 && (p.N & 3) == 0) {
         __syncthreads();   // every wave is done reading the stages
-        constexpr int TS = 68;   // region row stride in floats (64 + 4 keeps the accesses conflict-free)
+        constexpr int TS = 68, TSB = 72;
         float* const tl = (float*)lds + wave * (64 * TS);
+        uint16_t* const tlb = (uint16_t*)tl;
         const int64_t colg = n0 + wn * 64 + 4 * (lane & 15);
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
@@ -689,24 +751,43 @@ __global__ __launch_bounds__(512, 2) void lut_gemm_big(GemmParams p, int ntm, in
             for (int ii = 0; ii < 2; ++ii) {
                 const int i = 2 * half + ii;
                 const float xs = xsv[i];
+                const int lrow = ii * 32 + (lane & 31);
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         const uint2 rw = rwv[j][q];
-                        *(float4*)(tl + (ii * 32 + (lane & 31)) * TS + j * 32 + 8 * q + 4 * (lane >> 5)) =
-                            make_float4(acc[i][j][4 * q + 0] * xs * __uint_as_float(rw.x << 16),
-                                        acc[i][j][4 * q + 1] * xs * __uint_as_float(rw.x & 0xFFFF0000u),
-                                        acc[i][j][4 * q + 2] * xs * __uint_as_float(rw.y << 16),
-                                        acc[i][j][4 * q + 3] * xs * __uint_as_float(rw.y & 0xFFFF0000u));
+                        float v[4] = {acc[i][j][4 * q + 0] * xs * __uint_as_float(rw.x << 16),
+                                      acc[i][j][4 * q + 1] * xs * __uint_as_float(rw.x & 0xFFFF0000u),
+                                      acc[i][j][4 * q + 2] * xs * __uint_as_float(rw.y << 16),
+                                      acc[i][j][4 * q + 3] * xs * __uint_as_float(rw.y & 0xFFFF0000u)};
+                        const int lcol = j * 32 + 8 * q + 4 * (lane >> 5);
+                        if (!plain) {
+                            const uint2 b = bv[j][q];
+                            v[0] = epilogue_value(p, v[0], __uint_as_float(b.x << 16));
+                            v[1] = epilogue_value(p, v[1], __uint_as_float(b.x & 0xFFFF0000u));
+                            v[2] = epilogue_value(p, v[2], __uint_as_float(b.y << 16));
+                            v[3] = epilogue_value(p, v[3], __uint_as_float(b.y & 0xFFFF0000u));
+                        }
+                        if (p.out_bf16)
+                            *(uint2*)(tlb + lrow * TSB + lcol) =
+                                make_uint2(f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16),
+                                           f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16));
+                        else
+                            *(float4*)(tl + lrow * TS + lcol) = make_float4(v[0], v[1], v[2], v[3]);
                     }
             }
 #pragma unroll
             for (int t = 0; t < 16; ++t) {
                 const int r = 4 * t + (lane >> 4);
-                const float4 v = *(const float4*)(tl + r * TS + 4 * (lane & 15));
                 const int64_t row = m0 + wm * 128 + 64 * half + r;
-                if (row < p.M && colg < p.N) *(float4*)((float*)p.Y + row * p.ldy + colg) = v;
+                if (p.out_bf16) {
+                    const uint2 v = *(const uint2*)(tlb + r * TSB + 4 * (lane & 15));
+                    if (row < p.M && colg < p.N) *(uint2*)((uint16_t*)p.Y + row * p.ldy + colg) = v;
+                } else {
+                    const float4 v = *(const float4*)(tl + r * TS + 4 * (lane & 15));
+                    if (row < p.M && colg < p.N) *(float4*)((float*)p.Y + row * p.ldy + colg) = v;
+                }
             }
         }
         return;
