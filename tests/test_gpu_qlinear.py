@@ -77,8 +77,9 @@ def test_random_codes_large_tiles(M, N, K, ba, bw):
 
 
 # the fused layer epilogue (bias, GELU, bf16 output) on both kernels, with vector and element-wise
-# stores (ldy a multiple of 4 or not)
-@pytest.mark.parametrize("M,N,K", [(300, 130, 512), (4133, 8061, 192)])
+# stores (ldy a multiple of 4 or not); with N and ldy multiples of 4 the outputs go through the
+# kernels' LDS turn-around
+@pytest.mark.parametrize("M,N,K", [(300, 130, 512), (4133, 8061, 192), (300, 132, 512), (4133, 8064, 192)])
 @pytest.mark.parametrize("bias,gelu,bf16", [(True, False, False), (False, True, False), (False, False, True),
                                             (True, True, True)])
 @pytest.mark.parametrize("pad", [0, 1])

@@ -114,8 +114,9 @@ def test_split_remaining_bit_pairs(M, N, K, ba, bw):
 @pytest.mark.parametrize("bias,gelu,bf16", [(True, False, False), (False, True, False), (False, False, True),
                                             (True, True, True)])
 @pytest.mark.parametrize("pad", [0, 1])
-def test_split_fused_epilogue(bias, gelu, bf16, pad):
-    M, N, K, ba, bw = 200, 390, 2048, 4, 4
+@pytest.mark.parametrize("N", [390, 392])   # 392 with pad 0: the partial sums and Y through LDS
+def test_split_fused_epilogue(bias, gelu, bf16, pad, N):
+    M, K, ba, bw = 200, 2048, 4, 4
     host, (cba, cbw), (xp, xs, wp, wr) = _operands(M, N, K, ba, bw, seed=11)
     n, ws = _workspace(M, N, K)
     assert _splits(M, N, K, n) >= 2
