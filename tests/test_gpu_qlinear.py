@@ -266,3 +266,31 @@ def test_empty_operands_are_noops():
     Y = oq.orbit_qlinear_ex(cb, xc1, xn1, cb, wc[:0], wn[:0], gelu=True, out_dtype=torch.bfloat16)
     torch.cuda.synchronize()
     assert Y.shape == (8, 0)
+
+
+# The two store paths of both GEMM kernels hold the same values: with N and ldy multiples of 4 the
+# outputs are turned around in LDS before the stores, otherwise each lane stores its runs of four
+# columns directly.  Each output is the same arithmetic either way, so a layer written into rows of
+# N + 4 and into rows of N + 1 must agree bit for bit (large tiles, the 128 x 128 rows of a
+# partial last round, and a small grid; fp32 and the fused bias + GELU + bf16 epilogue).
+@pytest.mark.parametrize("M,N,K", [(4133, 8064, 192), (300, 132, 512)])
+@pytest.mark.parametrize("fused", [False, True])
+def test_store_paths_agree(M, N, K, fused):
+    ba, bw = 4, 4
+    xc, xs, wc, wr = _inputs(M, N, K, ba, bw, seed=M + 3 * N + K)
+    cba, cbw = oq.lloydmax_codebook(ba, K), oq.lloydmax_codebook(bw, K)
+    xp = torch.from_numpy(oracle.pack_codes(oracle.to_labels(xc.numpy(), ba), ba)).to(DEV)
+    wp = torch.from_numpy(oracle.pack_codes(oracle.to_labels(wc.numpy(), bw), bw)).to(DEV)
+    g = torch.Generator()
+    g.manual_seed(N + 1)
+    b = torch.randn(N, generator=g).to(torch.bfloat16).to(DEV) if fused else None
+    dt = torch.bfloat16 if fused else torch.float32
+    outs = []
+    for pad in (4, 1):
+        out = torch.full((M, N + pad), float("nan"), dtype=dt, device=DEV)[:, :N]
+        oq.orbit_qlinear_ex(cba, xp, xs.to(DEV), cbw, wp, wr.to(DEV), bias=b, gelu=fused, out_dtype=dt, out=out)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert not torch.isnan(outs[0].float()).any() and not torch.isnan(outs[1].float()).any()
+    assert torch.equal(outs[0].view(torch.int16) if fused else outs[0].view(torch.int32),
+                       outs[1].view(torch.int16) if fused else outs[1].view(torch.int32))
